@@ -1,0 +1,279 @@
+"""CPU oracle for two-sided adaptive rounding (GPTQ-2D, arXiv 2607.27042).
+
+TEST INFRASTRUCTURE ONLY. Only the test suite, ``__graft_entry__.smoke()`` and
+the ``cpu_baseline`` leg of ``bench.py`` may import this package. The product
+library never links, loads or calls it, and it shares no code with the GPU path.
+
+This module is argument marshalling around ``oracle.c`` (plain C, fp64):
+
+* ``gram_left`` / ``gram_right``  -- G = A^T A, H = B B^T (Sec. 3.2, Eq. GH)
+* ``feedback``                    -- unit-lower LDL factor of an inverse Gram,
+                                     by explicit inverse then LDL (Sec. 3.1)
+* ``factors``                     -- per-axis L, U of the two-sided problem
+                                     (Sec. 4.1)
+* ``round_1d``                    -- Algorithm 1
+* ``round_quartic``               -- Algorithm 1 on vec(X) under an explicit
+                                     Kronecker Gram H (x) G (Eq. kron-objective)
+* ``round_kron``                  -- Algorithm 1 on vec(X) with F = U^T (x) L
+                                     (Eq. vectorized-feedback)
+* ``round_nested``                -- Algorithm 5, the cubic oracle (Appendix A)
+* ``round_nested_corner``         -- Algorithm 5 on a leading block
+* ``round_gptq2d``                -- Algorithm 3 (Sec. 4.2)
+* ``round_implicit``              -- Algorithm 6 (Appendix B)
+* ``objective``                   -- ||A (Z - X) B||_F^2 by definition
+
+Every sweep returns ``(Z, Ypre, counts, hard)``: the rounded matrix (int32),
+the value each entry had when it was rounded, the synchronised-replay counters
+``{"window", "hard", "range"}`` and the flat indices of the first hard
+mismatches.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile ``oracle.c`` into ``liboracle.so`` with gcc and OpenMP."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB)
+        dp = ctypes.POINTER(ctypes.c_double)
+        ip = ctypes.POINTER(ctypes.c_int32)
+        lp = ctypes.POINTER(ctypes.c_int64)
+        i = ctypes.c_int
+        lib.orc_gram_left.argtypes = [i, dp, dp]
+        lib.orc_gram_right.argtypes = [i, dp, dp]
+        lib.orc_inverse.argtypes = [i, dp, dp]
+        lib.orc_inverse.restype = i
+        lib.orc_ldl.argtypes = [i, dp, dp, dp]
+        lib.orc_ldl.restype = i
+        lib.orc_feedback.argtypes = [i, dp, dp, dp]
+        lib.orc_feedback.restype = i
+        lib.orc_factors.argtypes = [i, i, dp, dp, dp, dp, dp, dp]
+        lib.orc_factors.restype = i
+        lib.orc_round_1d.argtypes = [i, dp, dp, ip, ctypes.c_double, ip, dp, lp, lp, i]
+        lib.orc_round_1d.restype = i
+        lib.orc_round_quartic.argtypes = [i, i, dp, dp, dp, ip, ctypes.c_double, ip, dp, lp, lp, i]
+        lib.orc_round_quartic.restype = i
+        for name in ("orc_round_kron", "orc_round_nested", "orc_round_gptq2d", "orc_round_implicit"):
+            f = getattr(lib, name)
+            f.argtypes = [i, i, dp, dp, dp, ip, ctypes.c_double, ip, dp, lp, lp, i]
+            f.restype = i
+        lib.orc_round_nested_corner.argtypes = [i, i, i, i, dp, dp, dp, ip, ctypes.c_double, ip, dp,
+                                                lp, lp, i]
+        lib.orc_round_nested_corner.restype = i
+        lib.orc_objective.argtypes = [i, i, dp, ip, dp, dp]
+        lib.orc_objective.restype = ctypes.c_double
+        lib.orc_num_threads.argtypes = []
+        lib.orc_num_threads.restype = i
+        _lib = lib
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+_STATUS = {0: "ok", -2: "singular or not positive definite", -4: "out of memory",
+           -7: "rounded value outside int32"}
+
+
+def _check(st: int, what: str):
+    if st != 0:
+        raise OracleError(f"{what}: {_STATUS.get(st, st)}")
+
+
+def _d(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _dp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _ip(a):
+    if a is None:
+        return ctypes.cast(None, ctypes.POINTER(ctypes.c_int32))
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _lp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def num_threads() -> int:
+    return int(_load().orc_num_threads())
+
+
+def gram_left(A) -> np.ndarray:
+    A = _d(A)
+    m = A.shape[0]
+    G = np.empty((m, m))
+    _load().orc_gram_left(m, _dp(A), _dp(G))
+    return G
+
+
+def gram_right(B) -> np.ndarray:
+    B = _d(B)
+    n = B.shape[0]
+    H = np.empty((n, n))
+    _load().orc_gram_right(n, _dp(B), _dp(H))
+    return H
+
+
+def inverse(M) -> np.ndarray:
+    M = _d(M)
+    d = M.shape[0]
+    out = np.empty((d, d))
+    _check(_load().orc_inverse(d, _dp(M), _dp(out)), "inverse")
+    return out
+
+
+def ldl(S):
+    S = _d(S)
+    d = S.shape[0]
+    F = np.empty((d, d))
+    D = np.empty(d)
+    _check(_load().orc_ldl(d, _dp(S), _dp(F), _dp(D)), "ldl")
+    return F, D
+
+
+def feedback(Q):
+    """Unit-lower F and diagonal lam with Q^{-1} = F diag(lam) F^T."""
+    Q = _d(Q)
+    d = Q.shape[0]
+    F = np.empty((d, d))
+    lam = np.empty(d)
+    _check(_load().orc_feedback(d, _dp(Q), _dp(F), _dp(lam)), "feedback")
+    return F, lam
+
+
+def factors(A, B):
+    """(L, lamL, U, lamU) for the bases A (m x m) and B (n x n)."""
+    A = _d(A)
+    B = _d(B)
+    m, n = A.shape[0], B.shape[0]
+    L = np.empty((m, m))
+    U = np.empty((n, n))
+    lamL = np.empty(m)
+    lamU = np.empty(n)
+    _check(_load().orc_factors(m, n, _dp(A), _dp(B), _dp(L), _dp(lamL), _dp(U), _dp(lamU)),
+           "factors")
+    return L, lamL, U, lamU
+
+
+def _replay_args(hint, shape, tau, hard_cap):
+    h = None if hint is None else np.ascontiguousarray(hint, dtype=np.int32)
+    if h is not None and h.shape != shape:
+        raise ValueError("hint shape mismatch")
+    counts = np.zeros(3, dtype=np.int64)
+    hard = np.zeros(max(hard_cap, 1), dtype=np.int64)
+    return h, counts, hard
+
+
+def _result(Z, Y, counts, hard, hard_cap):
+    c = {"window": int(counts[0]), "hard": int(counts[1]), "range": int(counts[2])}
+    return Z, Y, c, hard[: min(c["hard"], hard_cap)].copy()
+
+
+def round_1d(x, F, hint=None, tau=0.0, hard_cap=64):
+    x = _d(x)
+    F = _d(F)
+    d = x.shape[0]
+    h, counts, hard = _replay_args(hint, (d,), tau, hard_cap)
+    z = np.empty(d, dtype=np.int32)
+    y = np.empty(d)
+    _check(_load().orc_round_1d(d, _dp(x), _dp(F), _ip(h), float(tau), _ip(z), _dp(y), _lp(counts),
+                                _lp(hard), hard_cap), "round_1d")
+    return _result(z, y, counts, hard, hard_cap)
+
+
+def round_quartic(X, A, B, hint=None, tau=0.0, hard_cap=64):
+    X = _d(X)
+    A = _d(A)
+    B = _d(B)
+    m, n = X.shape
+    h, counts, hard = _replay_args(hint, (m, n), tau, hard_cap)
+    Z = np.empty((m, n), dtype=np.int32)
+    Y = np.empty((m, n))
+    _check(_load().orc_round_quartic(m, n, _dp(X), _dp(A), _dp(B), _ip(h), float(tau), _ip(Z),
+                                     _dp(Y), _lp(counts), _lp(hard), hard_cap), "round_quartic")
+    return _result(Z, Y, counts, hard, hard_cap)
+
+
+def _sweep(name, X, L, U, hint, tau, hard_cap):
+    X = _d(X)
+    L = _d(L)
+    U = _d(U)
+    m, n = X.shape
+    if L.shape != (m, m) or U.shape != (n, n):
+        raise ValueError("factor shape mismatch")
+    h, counts, hard = _replay_args(hint, (m, n), tau, hard_cap)
+    Z = np.empty((m, n), dtype=np.int32)
+    Y = np.empty((m, n))
+    f = getattr(_load(), name)
+    _check(f(m, n, _dp(X), _dp(L), _dp(U), _ip(h), float(tau), _ip(Z), _dp(Y), _lp(counts),
+             _lp(hard), hard_cap), name)
+    return _result(Z, Y, counts, hard, hard_cap)
+
+
+def round_kron(X, L, U, hint=None, tau=0.0, hard_cap=64):
+    return _sweep("orc_round_kron", X, L, U, hint, tau, hard_cap)
+
+
+def round_nested(X, L, U, hint=None, tau=0.0, hard_cap=64):
+    return _sweep("orc_round_nested", X, L, U, hint, tau, hard_cap)
+
+
+def round_gptq2d(X, L, U, hint=None, tau=0.0, hard_cap=64):
+    return _sweep("orc_round_gptq2d", X, L, U, hint, tau, hard_cap)
+
+
+def round_implicit(X, L, U, hint=None, tau=0.0, hard_cap=64):
+    return _sweep("orc_round_implicit", X, L, U, hint, tau, hard_cap)
+
+
+def round_nested_corner(X, L, U, m1, n1, hint=None, tau=0.0, hard_cap=64):
+    """Algorithm 5 on the leading m1 x n1 block of the full problem."""
+    X = _d(X)
+    L = _d(L)
+    U = _d(U)
+    m, n = X.shape
+    if not (0 < m1 <= m and 0 < n1 <= n):
+        raise ValueError("corner out of range")
+    h, counts, hard = _replay_args(hint, (m1, n1), tau, hard_cap)
+    Z = np.empty((m1, n1), dtype=np.int32)
+    Y = np.empty((m1, n1))
+    _check(_load().orc_round_nested_corner(m, n, m1, n1, _dp(X), _dp(L), _dp(U), _ip(h), float(tau),
+                                           _ip(Z), _dp(Y), _lp(counts), _lp(hard), hard_cap),
+           "round_nested_corner")
+    return _result(Z, Y, counts, hard, hard_cap)
+
+
+def objective(X, Z, A, B) -> float:
+    X = _d(X)
+    Z = np.ascontiguousarray(Z, dtype=np.int32)
+    A = _d(A)
+    B = _d(B)
+    m, n = X.shape
+    return float(_load().orc_objective(m, n, _dp(X), _ip(Z), _dp(A), _dp(B)))

@@ -1,0 +1,347 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these checks re-types an oracle formula: each compares the oracle with
+an independent route (a library factorisation, a textbook algorithm in its own
+standard form, a brute-force search, a closed form, an invariant of the
+trajectory) chosen so that a dropped term, a wrong sign, a transposed operand
+or a wrong vectorisation order fails at least one of them.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import scipy.linalg as sla
+
+import oracle
+from paper_2607_27042_amd import workloads as wl
+
+SHAPES = [(1, 1), (1, 5), (6, 1), (2, 3), (5, 4), (7, 7), (9, 13), (16, 11), (24, 24)]
+
+
+def _prob(m, n, seed, kind="wishart"):
+    p = wl.random_problem(m, n, seed, "f64", kind)
+    return p.widened()
+
+
+# --------------------------------------------------------------------------
+# Factors (Sec. 3.1, Sec. 4.1)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d", [1, 2, 5, 17, 40])
+def test_feedback_is_ldl_of_inverse(d):
+    """F unit lower and F diag(lam) F^T Q = I (checked through Q, not Q^{-1})."""
+    rng = np.random.default_rng(d)
+    W = rng.standard_normal((3 * d, d))
+    Q = W.T @ W / (3 * d) + 0.1 * np.eye(d)
+    F, lam = oracle.feedback(Q)
+    assert np.array_equal(np.diag(F), np.ones(d))
+    assert np.abs(np.triu(F, 1)).max(initial=0.0) == 0.0
+    assert (lam > 0).all()
+    R = F @ np.diag(lam) @ F.T @ Q
+    assert np.abs(R - np.eye(d)).max() < 1e-11
+
+
+@pytest.mark.parametrize("d", [1, 3, 8, 31])
+def test_feedback_matches_textbook_gptq_cholesky(d):
+    """GPTQ's construction: upper Cholesky R of Q^{-1} (numpy), F = R^T diag(R)^{-1}."""
+    rng = np.random.default_rng(100 + d)
+    W = rng.standard_normal((2 * d + 3, d))
+    Q = W.T @ W + 0.5 * np.eye(d)
+    R = np.linalg.cholesky(np.linalg.inv(Q)).T  # upper, Q^{-1} = R^T R
+    F_ref = R.T / np.diag(R)[None, :]
+    F, lam = oracle.feedback(Q)
+    np.testing.assert_allclose(F, F_ref, rtol=0, atol=1e-11 * max(1.0, np.abs(F_ref).max()))
+    np.testing.assert_allclose(lam, np.diag(R) ** 2, rtol=1e-11)
+
+
+@pytest.mark.parametrize("m,n", [(1, 1), (4, 6), (13, 9), (30, 30)])
+def test_factor_closed_form_triangular(m, n):
+    """A lower => L = A^{-1} diag(A), lamL = diag(A)^{-2};
+    B upper => U = diag(B) B^{-1}, lamU = diag(B)^{-2} (triangular solves)."""
+    X, A, B = _prob(m, n, 7, "lower")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Lref = sla.solve_triangular(A, np.diag(np.diag(A)), lower=True)
+    Uref = np.diag(np.diag(B)) @ sla.solve_triangular(B, np.eye(n), lower=False)
+    np.testing.assert_allclose(L, Lref, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(U, Uref, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lamL, np.diag(A) ** -2.0, rtol=1e-12)
+    np.testing.assert_allclose(lamU, np.diag(B) ** -2.0, rtol=1e-12)
+
+
+def test_factor_diagonal_is_identity():
+    X, A, B = _prob(6, 9, 3, "diag")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    np.testing.assert_allclose(L, np.eye(6), atol=1e-15)
+    np.testing.assert_allclose(U, np.eye(9), atol=1e-15)
+    np.testing.assert_allclose(lamL, np.diag(A) ** -2.0, rtol=1e-13)
+    np.testing.assert_allclose(lamU, np.diag(B) ** -2.0, rtol=1e-13)
+
+
+def test_factor_config5_upper_B_closed_form():
+    """Config 5's bases are upper triangular: U is pinned by back-substitution.
+    (Config 5's basis recipe at d = 256.)"""
+    B = wl._basis_c5(256, np.random.default_rng([5, 2]))
+    A = wl._basis_c5(256, np.random.default_rng([5, 1]))
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Uref = np.diag(np.diag(B)) @ sla.solve_triangular(B, np.eye(256), lower=False)
+    np.testing.assert_allclose(U, Uref, rtol=0, atol=1e-10)
+    np.testing.assert_allclose(lamU, np.diag(B) ** -2.0, rtol=1e-10)
+
+
+def test_factor_singular_is_reported():
+    A = np.ones((4, 4))
+    with pytest.raises(oracle.OracleError):
+        oracle.factors(A, np.eye(3))
+
+
+# --------------------------------------------------------------------------
+# Trajectory: every realisation gives the same Z (Theorems 1 and 2)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("m,n", SHAPES)
+@pytest.mark.parametrize("kind", ["wishart", "general"])
+def test_all_realisations_agree(m, n, kind):
+    X, A, B = _prob(m, n, 11, kind)
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zq, Yq, _, _ = oracle.round_quartic(X, A, B)
+    for fn in (oracle.round_kron, oracle.round_nested, oracle.round_gptq2d,
+               oracle.round_implicit):
+        Z, Y, c, _ = fn(X, L, U)
+        assert np.array_equal(Z, Zq), fn.__name__
+        assert np.abs(Y - Yq).max() < 1e-9, fn.__name__
+
+
+def test_config1_quartic_equals_cubic():
+    """Config 1 (64 x 64 fp64): the explicit 4096 x 4096 Kronecker sweep and the
+    nested cubic sweep produce the identical Z (Theorem 2)."""
+    X, A, B = wl.make_config(1).widened()
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zc, Yc, _, _ = oracle.round_nested(X, L, U)
+    Zq, Yq, _, _ = oracle.round_quartic(X, A, B)
+    assert np.array_equal(Zc, Zq)
+    assert np.abs(Yc - Yq).max() < 1e-10
+
+
+def test_config2_kron_equals_cubic():
+    """Config 2 (512 x 384): Algorithm 1 with F = U^T (x) L generated from the
+    per-axis factors equals the nested sweep."""
+    X, A, B = wl.make_config(2).widened()
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zc, Yc, _, _ = oracle.round_nested(X, L, U)
+    Zk, Yk, _, _ = oracle.round_kron(X, L, U)
+    assert np.array_equal(Zc, Zk)
+    assert np.abs(Yc - Yk).max() < 1e-9
+
+
+# --------------------------------------------------------------------------
+# Special cases that reduce to textbook routines
+# --------------------------------------------------------------------------
+
+def _textbook_gptq(w, Hs):
+    """GPTQ's loop in its usual form on one weight vector w under Hessian Hs."""
+    w = np.array(w, dtype=np.float64)
+    R = np.linalg.cholesky(np.linalg.inv(Hs)).T
+    q = np.empty(len(w))
+    for k in range(len(w)):
+        q[k] = np.rint(w[k])
+        err = (w[k] - q[k]) / R[k, k]
+        w[k:] -= err * R[k, k:]
+    return q.astype(np.int32)
+
+
+@pytest.mark.parametrize("m,n", [(1, 4), (8, 3), (20, 7)])
+def test_right_identity_is_columnwise_gptq(m, n):
+    """B = I: each column is rounded by one-sided GPTQ under G = A^T A."""
+    X, A, B = _prob(m, n, 5, "identity_right")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    G = A.T @ A
+    for j in range(n):
+        assert np.array_equal(Z[:, j], _textbook_gptq(X[:, j], G))
+
+
+@pytest.mark.parametrize("m,n", [(4, 1), (3, 8), (7, 20)])
+def test_left_identity_is_rowwise_gptq(m, n):
+    """A = I: each row is rounded by one-sided GPTQ under H = B B^T (row mirror)."""
+    X, A, B = _prob(m, n, 6, "identity_left")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_gptq2d(X, L, U)
+    H = B @ B.T
+    for i in range(m):
+        assert np.array_equal(Z[i, :], _textbook_gptq(X[i, :], H))
+
+
+def test_diagonal_bases_round_to_nearest():
+    X, A, B = _prob(11, 6, 9, "diag")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    for fn in (oracle.round_nested, oracle.round_gptq2d, oracle.round_implicit):
+        Z, Y, _, _ = fn(X, L, U)
+        assert np.array_equal(Z, np.rint(X).astype(np.int32))
+        assert np.abs(Y - X).max() < 1e-14
+    Zq, _, _, _ = oracle.round_quartic(X, A, B)
+    assert np.array_equal(Zq, np.rint(X).astype(np.int32))
+    a, b = np.diag(A), np.diag(B)
+    obj = np.sum((a[:, None] * b[None, :] * (np.rint(X) - X)) ** 2)
+    assert abs(oracle.objective(X, Zq, A, B) - obj) <= 1e-12 * obj
+
+
+def test_ties_break_to_even():
+    X = np.array([[0.5, 1.5, 2.5, -0.5, -1.5, -2.5]])
+    Z, Y, _, _ = oracle.round_nested(X, np.eye(1), np.eye(6))
+    assert Z.tolist() == [[0, 2, 2, 0, -2, -2]]
+
+
+# --------------------------------------------------------------------------
+# Brute-force greedy (Babai nearest plane) on tiny problems
+# --------------------------------------------------------------------------
+
+def _kron_metric(A, B):
+    """K with vec(R)^T K vec(R) = ||A R B||_F^2, built from the definition by
+    applying the map R -> A R B to every basis matrix (column-major vec)."""
+    m, n = A.shape[0], B.shape[0]
+    M = np.empty((m * n, m * n))
+    for k in range(m * n):
+        E = np.zeros((m, n))
+        E[k % m, k // m] = 1.0
+        M[:, k] = (A @ E @ B).reshape(-1, order="F")
+    return M.T @ M
+
+
+def _greedy_bruteforce(X, A, B):
+    m, n = X.shape
+    K = _kron_metric(A, B)
+    x = X.reshape(-1, order="F")
+    d = m * n
+    z = np.zeros(d)
+    cont = np.zeros(d)
+    for k in range(d):
+        a = np.arange(k + 1)
+        b = np.arange(k + 1, d)
+        S = K[np.ix_(a, a)]
+        if len(b):
+            S = S - K[np.ix_(a, b)] @ np.linalg.solve(K[np.ix_(b, b)], K[np.ix_(b, a)])
+        r_prev = z[:k] - x[:k]
+
+        def f(t):
+            r = np.append(r_prev, t - x[k])
+            return r @ S @ r
+
+        cont[k] = x[k] - (S[k, :k] @ r_prev) / S[k, k]
+        cands = np.arange(np.floor(cont[k]) - 2, np.ceil(cont[k]) + 3)
+        vals = np.array([f(t) for t in cands])
+        best = cands[np.isclose(vals, vals.min(), rtol=1e-12, atol=1e-12)]
+        z[k] = best[0] if len(best) == 1 else best[best % 2 == 0][0]
+    return z.reshape(m, n, order="F").astype(np.int32), cont.reshape(m, n, order="F")
+
+
+@pytest.mark.parametrize("m,n", list(itertools.product([1, 2, 3], [1, 2, 3])))
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_greedy_bruteforce(m, n, seed):
+    """Each entry, in column-major order, is the integer that minimises the
+    objective with earlier entries fixed and later ones free (Babai's greedy
+    step), and the value it is rounded from is that conditional minimiser."""
+    X, A, B = _prob(m, n, 40 + seed, "general")
+    Zb, contb = _greedy_bruteforce(X, A, B)
+    Zq, Yq, _, _ = oracle.round_quartic(X, A, B)
+    assert np.array_equal(Zq, Zb)
+    np.testing.assert_allclose(Yq, contb, rtol=0, atol=1e-9)
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zc, Yc, _, _ = oracle.round_nested(X, L, U)
+    assert np.array_equal(Zc, Zb)
+
+
+def test_kron_metric_matches_definition():
+    X, A, B = _prob(3, 4, 1, "general")
+    K = _kron_metric(A, B)
+    R = np.random.default_rng(0).standard_normal((3, 4))
+    r = R.reshape(-1, order="F")
+    assert abs(r @ K @ r - np.linalg.norm(A @ R @ B) ** 2) < 1e-10
+
+
+# --------------------------------------------------------------------------
+# Invariants of the trajectory
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("m,n", [(5, 8), (17, 12), (32, 32)])
+def test_trajectory_invariants(m, n):
+    """Z - X = L E U with E = Z - Y (Eq. Y-LEU, final errors), |E| <= 1/2,
+    Z = rint(Y), and ||A(Z-X)B||^2 = sum E^2 / (lamL lamU)."""
+    X, A, B = _prob(m, n, 21, "wishart")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    E = Z - Y
+    assert np.abs(E).max() <= 0.5
+    assert np.array_equal(Z, np.rint(Y).astype(np.int32))
+    assert np.abs((Z - X) - L @ E @ U).max() < 1e-10
+    obj = oracle.objective(X, Z, A, B)
+    ident = float(np.sum(E * E / np.outer(lamL, lamU)))
+    assert abs(obj - ident) <= 1e-10 * obj
+    ref = np.linalg.norm(A @ (Z - X) @ B) ** 2
+    assert abs(obj - ref) <= 1e-10 * obj
+
+
+@pytest.mark.parametrize("m,n", [(6, 9), (14, 5)])
+def test_transposition(m, n):
+    """Rounding X^T under (B^T, A^T) is the same problem (Sec. 5): Z transposes."""
+    X, A, B = _prob(m, n, 31, "general")
+    L, _, U, _ = oracle.factors(A, B)
+    Z, _, _, _ = oracle.round_nested(X, L, U)
+    Lt, _, Ut, _ = oracle.factors(B.T, A.T)
+    Zt, _, _, _ = oracle.round_nested(X.T, Lt, Ut)
+    assert np.array_equal(Zt, Z.T)
+
+
+def test_scale_invariance():
+    X, A, B = _prob(9, 7, 8, "wishart")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    L2, lamL2, U2, lamU2 = oracle.factors(3.0 * A, B)
+    Z2, Y2, _, _ = oracle.round_nested(X, L2, U2)
+    assert np.array_equal(Z, Z2)
+    np.testing.assert_allclose(lamL2, lamL / 9.0, rtol=1e-12)
+    o1 = oracle.objective(X, Z, A, B)
+    o2 = oracle.objective(X, Z2, 3.0 * A, B)
+    assert abs(o2 - 9.0 * o1) <= 1e-12 * o2
+
+
+def test_corner_is_self_contained():
+    X, A, B = _prob(20, 26, 4, "wishart")
+    L, _, U, _ = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    Zc, Yc, _, _ = oracle.round_nested_corner(X, L, U, 9, 13)
+    assert np.array_equal(Zc, Z[:9, :13])
+    assert np.abs(Yc - Y[:9, :13]).max() < 1e-12
+
+
+# --------------------------------------------------------------------------
+# Synchronised replay
+# --------------------------------------------------------------------------
+
+def test_replay_counts_window_and_hard():
+    X = np.array([[2.5, 0.2, -1.5], [3.49, 1.0, 0.75]])
+    L = np.eye(2)
+    U = np.eye(3)
+    Z, Y, c, _ = oracle.round_nested(X, L, U)
+    assert c == {"window": 0, "hard": 0, "range": 0}
+    hint = Z.copy()
+    hint[0, 0] = 3   # 2.5 is a tie: inside any window
+    hint[0, 2] = -1  # -1.5 is a tie as well
+    hint[1, 1] = 2   # 1.0 is far from the half-integer 1.5: hard
+    Zr, Yr, c, hard = oracle.round_nested(X, L, U, hint=hint, tau=1e-12)
+    assert c["window"] == 2 and c["hard"] == 1
+    assert hard.tolist() == [1 * 3 + 1]
+    assert np.array_equal(Zr, hint)
+
+
+def test_replay_follows_hint_trajectory():
+    """After a hinted flip, later entries are computed on the hinted
+    trajectory, exactly as a sweep that rounded that entry the other way."""
+    X, A, B = _prob(6, 6, 2, "wishart")
+    L, _, U, _ = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    hint = Z.copy()
+    hint[0, 0] += 1
+    Zr, Yr, c, hard = oracle.round_nested(X, L, U, hint=hint, tau=0.0)
+    assert c["hard"] >= 1 and hard[0] == 0
+    E = Zr - Yr
+    assert np.abs((Zr - X) - L @ E @ U).max() < 1e-10
