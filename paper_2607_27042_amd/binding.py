@@ -1,0 +1,296 @@
+"""Thin Python binding of ``libgptq2d.so`` (the C ABI in ``include/gptq2d.h``).
+
+Argument marshalling only: every step of the factorisation and of the sweep
+runs in the library's HIP kernels. PyTorch supplies device memory and the
+current stream. The library must be built (``__graft_entry__.build()``); a
+missing library is an error, never a fallback.
+
+The functions named like the C entry points take and return the same things,
+with torch tensors in place of device pointers and Python ints in place of
+handles. ``Factors`` and ``round_matrix`` are conveniences built from them.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "lib", "libgptq2d.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "gptq2d.h")
+
+F32, F64 = 0, 1
+STATUS = {0: "OK", -1: "ERR_INVALID_ARG", -2: "ERR_SINGULAR", -3: "ERR_NONFINITE", -4: "ERR_OOM",
+          -5: "ERR_HIP", -6: "ERR_WORKSPACE", -7: "ERR_OVERFLOW"}
+
+_lib = None
+
+
+class Gptq2dError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {detail}")
+
+
+def declared_functions() -> list[str]:
+    """Names of the functions declared in include/gptq2d.h."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gptq2d_[a-z_]+)\s*\(", text)))
+
+
+def load():
+    """Load the built library (raises if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
+    ip32 = ctypes.POINTER(ctypes.c_int32)
+    sigs = {
+        "gptq2d_factors_create": (i32, [i32, i32, ctypes.POINTER(vp)]),
+        "gptq2d_factors_destroy": (None, [vp]),
+        "gptq2d_factors_shape": (i32, [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]),
+        "gptq2d_factor_compute": (i32, [vp, i32, vp, i64, vp, i64, vp]),
+        "gptq2d_factor_check": (i32, [vp, vp]),
+        "gptq2d_factor": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, ctypes.POINTER(vp)]),
+        "gptq2d_factors_export": (i32, [vp, vp, i64, vp, i64, vp, vp, vp]),
+        "gptq2d_factors_import": (i32, [vp, vp, i64, vp, i64, vp, vp, vp]),
+        "gptq2d_round_workspace_size": (sz, [vp]),
+        "gptq2d_round": (i32, [vp, i32, vp, i64, vp, i64, vp, i64, vp, vp, sz, vp]),
+        "gptq2d_round_check": (i32, [vp, vp, vp]),
+        "gptq2d_status_string": (ctypes.c_char_p, [i32]),
+        "gptq2d_last_error": (ctypes.c_char_p, []),
+        "gptq2d_version": (i32, []),
+        "gptq2d_schedule_tasks": (i64, [i32, i32, i32, ip32, i64, ip32]),
+    }
+    for name, (res, args) in sigs.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise Gptq2dError(st, where, load().gptq2d_last_error().decode())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.float64:
+        return F64
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _mat(t: torch.Tensor, rows: int, cols: int, what: str):
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if t.dim() != 2 or tuple(t.shape) != (rows, cols):
+        raise ValueError(f"{what} must be {rows} x {cols}, got {tuple(t.shape)}")
+    if t.stride(1) != 1 and cols > 1:
+        raise ValueError(f"{what} must be row-major with unit column stride")
+    ld = t.stride(0) if rows > 1 else cols
+    return ctypes.c_void_p(t.data_ptr()), int(max(ld, cols))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+# ---------------------------------------------------------------------------
+# C entry points
+# ---------------------------------------------------------------------------
+
+def gptq2d_version() -> int:
+    return int(load().gptq2d_version())
+
+
+def gptq2d_status_string(st: int) -> str:
+    return load().gptq2d_status_string(st).decode()
+
+
+def gptq2d_last_error() -> str:
+    return load().gptq2d_last_error().decode()
+
+
+def gptq2d_factors_create(m: int, n: int) -> int:
+    h = ctypes.c_void_p()
+    _check(load().gptq2d_factors_create(m, n, ctypes.byref(h)), "gptq2d_factors_create")
+    return h.value
+
+
+def gptq2d_factors_destroy(h: int) -> None:
+    load().gptq2d_factors_destroy(ctypes.c_void_p(h))
+
+
+def gptq2d_factors_shape(h: int):
+    m, n = ctypes.c_int(), ctypes.c_int()
+    _check(load().gptq2d_factors_shape(ctypes.c_void_p(h), ctypes.byref(m), ctypes.byref(n)),
+           "gptq2d_factors_shape")
+    return m.value, n.value
+
+
+def gptq2d_factor_compute(h: int, A: torch.Tensor, B: torch.Tensor, stream=None) -> None:
+    m, n = gptq2d_factors_shape(h)
+    if A.dtype != B.dtype:
+        raise TypeError("A and B must share a dtype")
+    pa, lda = _mat(A, m, m, "A")
+    pb, ldb = _mat(B, n, n, "B")
+    _check(load().gptq2d_factor_compute(ctypes.c_void_p(h), _dt(A), pa, lda, pb, ldb, _stream(stream)),
+           "gptq2d_factor_compute")
+
+
+def gptq2d_factor_check(h: int, stream=None) -> None:
+    _check(load().gptq2d_factor_check(ctypes.c_void_p(h), _stream(stream)), "gptq2d_factor_check")
+
+
+def gptq2d_factor(A: torch.Tensor, B: torch.Tensor, stream=None) -> int:
+    if A.dtype != B.dtype:
+        raise TypeError("A and B must share a dtype")
+    m, n = A.shape[0], B.shape[0]
+    pa, lda = _mat(A, m, m, "A")
+    pb, ldb = _mat(B, n, n, "B")
+    h = ctypes.c_void_p()
+    _check(load().gptq2d_factor(m, n, _dt(A), pa, lda, pb, ldb, _stream(stream), ctypes.byref(h)),
+           "gptq2d_factor")
+    return h.value
+
+
+def gptq2d_factors_export(h: int, stream=None):
+    m, n = gptq2d_factors_shape(h)
+    dev = torch.cuda.current_device()
+    L = torch.empty((m, m), dtype=torch.float64, device=dev)
+    U = torch.empty((n, n), dtype=torch.float64, device=dev)
+    lamL = torch.empty(m, dtype=torch.float64, device=dev)
+    lamU = torch.empty(n, dtype=torch.float64, device=dev)
+    _check(load().gptq2d_factors_export(ctypes.c_void_p(h), _ptr(L), m, _ptr(U), n, _ptr(lamL),
+                                        _ptr(lamU), _stream(stream)), "gptq2d_factors_export")
+    return L, U, lamL, lamU
+
+
+def gptq2d_factors_import(h: int, L, U, lamL, lamU, stream=None) -> None:
+    m, n = gptq2d_factors_shape(h)
+    for t in (L, U, lamL, lamU):
+        if t.dtype != torch.float64 or not t.is_cuda:
+            raise TypeError("factors must be float64 device tensors")
+    pl, ldl = _mat(L, m, m, "L")
+    pu, ldu = _mat(U, n, n, "U")
+    if lamL.numel() != m or lamU.numel() != n or not lamL.is_contiguous() or not lamU.is_contiguous():
+        raise ValueError("lamL / lamU have the wrong size or layout")
+    _check(load().gptq2d_factors_import(ctypes.c_void_p(h), pl, ldl, pu, ldu, _ptr(lamL), _ptr(lamU),
+                                        _stream(stream)), "gptq2d_factors_import")
+
+
+def gptq2d_round_workspace_size(h: int) -> int:
+    return int(load().gptq2d_round_workspace_size(ctypes.c_void_p(h)))
+
+
+def gptq2d_round(h: int, X: torch.Tensor, Z: torch.Tensor, Y, objective, workspace: torch.Tensor,
+                 stream=None) -> None:
+    m, n = gptq2d_factors_shape(h)
+    px, ldx = _mat(X, m, n, "X")
+    if Z.dtype != torch.int32:
+        raise TypeError("Z must be int32")
+    pz, ldz = _mat(Z, m, n, "Z")
+    if Y is not None:
+        if Y.dtype != X.dtype:
+            raise TypeError("Y must have X's dtype")
+        py, ldy = _mat(Y, m, n, "Y")
+    else:
+        py, ldy = ctypes.c_void_p(0), n
+    if objective is not None and (objective.dtype != torch.float64 or not objective.is_cuda):
+        raise TypeError("objective must be a float64 device tensor")
+    _check(load().gptq2d_round(ctypes.c_void_p(h), _dt(X), px, ldx, pz, ldz, py, ldy, _ptr(objective),
+                               _ptr(workspace), workspace.numel() * workspace.element_size(),
+                               _stream(stream)), "gptq2d_round")
+
+
+def gptq2d_round_check(h: int, workspace: torch.Tensor, stream=None) -> None:
+    _check(load().gptq2d_round_check(ctypes.c_void_p(h), _ptr(workspace), _stream(stream)),
+           "gptq2d_round_check")
+
+
+def gptq2d_schedule_tasks(m: int, n: int, g: int):
+    """Host-only delivery plan: (tasks int32[T, 4], offsets int32[MT+NT])."""
+    import numpy as np
+    lib = load()
+    total = lib.gptq2d_schedule_tasks(m, n, g, None, 0, None)
+    if total < 0:
+        raise ValueError(gptq2d_last_error())
+    mt, nt = (m + 63) // 64, (n + 63) // 64
+    offs = np.zeros(mt + nt, dtype=np.int32)
+    tasks = np.zeros((max(total, 1), 4), dtype=np.int32)
+    lib.gptq2d_schedule_tasks(m, n, g, tasks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), total,
+                              offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
+    return tasks[:total], offs
+
+
+# ---------------------------------------------------------------------------
+# Conveniences
+# ---------------------------------------------------------------------------
+
+class Factors:
+    """Owning wrapper of a factor handle."""
+
+    def __init__(self, m: int, n: int):
+        self.m, self.n = m, n
+        self.handle = gptq2d_factors_create(m, n)
+
+    @classmethod
+    def from_bases(cls, A: torch.Tensor, B: torch.Tensor, check: bool = True, stream=None):
+        f = cls(A.shape[0], B.shape[0])
+        f.compute(A, B, stream)
+        if check:
+            gptq2d_factor_check(f.handle, stream)
+        return f
+
+    def compute(self, A, B, stream=None):
+        gptq2d_factor_compute(self.handle, A, B, stream)
+
+    def export(self, stream=None):
+        return gptq2d_factors_export(self.handle, stream)
+
+    def load(self, L, U, lamL, lamU, stream=None):
+        gptq2d_factors_import(self.handle, L, U, lamL, lamU, stream)
+
+    def workspace(self) -> torch.Tensor:
+        return torch.empty(gptq2d_round_workspace_size(self.handle), dtype=torch.uint8,
+                           device=torch.cuda.current_device())
+
+    def close(self):
+        if getattr(self, "handle", None):
+            gptq2d_factors_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def round_matrix(f: Factors, X: torch.Tensor, want_y: bool = True, workspace=None, check=True,
+                 stream=None):
+    """Z (int32), Y (X's dtype or None) and the objective (float64 device scalar)."""
+    m, n = f.m, f.n
+    Z = torch.empty((m, n), dtype=torch.int32, device=X.device)
+    Y = torch.empty((m, n), dtype=X.dtype, device=X.device) if want_y else None
+    obj = torch.empty(1, dtype=torch.float64, device=X.device)
+    ws = workspace if workspace is not None else f.workspace()
+    gptq2d_round(f.handle, X, Z, Y, obj, ws, stream)
+    if check:
+        gptq2d_round_check(f.handle, ws, stream)
+    return Z, Y, obj

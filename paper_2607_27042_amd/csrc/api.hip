@@ -1,0 +1,268 @@
+// C ABI of the library: argument validation, handle management and status
+// reporting around the factorisation and sweep launches.
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "device.hpp"
+#include "internal.hpp"
+
+struct gptq2d_factors_s : g2d::Factors {};
+
+namespace g2d {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+gptq2d_status hip_fail(hipError_t e, const char* what) {
+  set_error(std::string(what) + ": " + hipGetErrorString(e));
+  return e == hipErrorOutOfMemory ? GPTQ2D_ERR_OOM : GPTQ2D_ERR_HIP;
+}
+
+static gptq2d_status fail(gptq2d_status s, const std::string& msg) {
+  set_error(msg);
+  return s;
+}
+
+static int round_up(int v, int a) { return (v + a - 1) / a * a; }
+
+static void free_all(Factors* f) {
+  for (void* p : f->allocations) (void)hipFree(p);
+  f->allocations.clear();
+  if (f->sched.d_tasks) (void)hipFree(f->sched.d_tasks);
+  f->sched.d_tasks = nullptr;
+}
+
+static gptq2d_status alloc(Factors* f, void** p, size_t bytes) {
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) return hip_fail(e, "device allocation");
+  f->allocations.push_back(*p);
+  return GPTQ2D_OK;
+}
+
+static int env_int(const char* name, int def) {
+  const char* v = getenv(name);
+  if (!v || !*v) return def;
+  return atoi(v);
+}
+
+static gptq2d_status check_device(const Factors* f) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != f->device)
+    return fail(GPTQ2D_ERR_INVALID_ARG, "the current device is not the device of the handle");
+  return GPTQ2D_OK;
+}
+
+}  // namespace g2d
+
+using namespace g2d;
+
+extern "C" {
+
+gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
+  if (!out) return fail(GPTQ2D_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (m < 1 || n < 1 || m > 65536 || n > 65536)
+    return fail(GPTQ2D_ERR_INVALID_ARG, "m and n must lie in [1, 65536]");
+  gptq2d_factors_s* f = new gptq2d_factors_s();
+  f->m = m;
+  f->n = n;
+  f->mp = round_up(m, TB);
+  f->np = round_up(n, TB);
+  f->MT = f->mp / TB;
+  f->NT = f->np / TB;
+  hipError_t he = hipGetDevice(&f->device);
+  if (he != hipSuccess) {
+    delete f;
+    return hip_fail(he, "hipGetDevice");
+  }
+  const size_t mp = (size_t)f->mp, np = (size_t)f->np;
+  gptq2d_status st = GPTQ2D_OK;
+  void* p = nullptr;
+  auto A = [&](double** dst, size_t count) {
+    if (st != GPTQ2D_OK) return;
+    st = alloc(f, &p, count * sizeof(double));
+    if (st == GPTQ2D_OK) *dst = (double*)p;
+  };
+  A(&f->L, mp * mp);
+  A(&f->U, np * np);
+  A(&f->dL, mp);
+  A(&f->dU, np);
+  A(&f->gram[0], mp * mp);
+  A(&f->inv[0], mp * mp);
+  A(&f->dinv[0], mp * TB);
+  A(&f->gram[1], np * np);
+  A(&f->inv[1], np * np);
+  A(&f->dinv[1], np * TB);
+  if (st == GPTQ2D_OK) {
+    st = alloc(f, &p, 256);
+    if (st == GPTQ2D_OK) {
+      f->flags = (int*)p;
+      he = hipMemset(f->flags, 0, 256);
+      if (he != hipSuccess) st = hip_fail(he, "hipMemset");
+    }
+  }
+  if (st == GPTQ2D_OK) st = build_schedule(*f, env_int("GPTQ2D_BATCH", 4));
+  if (st != GPTQ2D_OK) {
+    free_all(f);
+    delete f;
+    return st;
+  }
+  *out = f;
+  return GPTQ2D_OK;
+}
+
+void gptq2d_factors_destroy(gptq2d_factors_t f) {
+  if (!f) return;
+  free_all(f);
+  delete f;
+}
+
+gptq2d_status gptq2d_factors_shape(gptq2d_factors_t f, int* m, int* n) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  if (m) *m = f->m;
+  if (n) *n = f->n;
+  return GPTQ2D_OK;
+}
+
+gptq2d_status gptq2d_factor_compute(gptq2d_factors_t f, gptq2d_dtype dt, const void* A,
+                                    int64_t lda, const void* B, int64_t ldb, void* stream) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  if (dt != GPTQ2D_F32 && dt != GPTQ2D_F64) return fail(GPTQ2D_ERR_INVALID_ARG, "bad dtype");
+  if (!A || !B) return fail(GPTQ2D_ERR_INVALID_ARG, "A or B is NULL");
+  if (lda < f->m || ldb < f->n) return fail(GPTQ2D_ERR_INVALID_ARG, "leading dimension too small");
+  gptq2d_status st = check_device(f);
+  if (st != GPTQ2D_OK) return st;
+  return launch_factor(*f, dt, A, lda, B, ldb, (hipStream_t)stream);
+}
+
+gptq2d_status gptq2d_factor_check(gptq2d_factors_t f, void* stream) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  int flags = 0;
+  e = hipMemcpy(&flags, f->flags, sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+  if (flags & FLAG_SINGULAR)
+    return fail(GPTQ2D_ERR_SINGULAR, "a Gram pivot was not positive and finite (A or B singular)");
+  return GPTQ2D_OK;
+}
+
+gptq2d_status gptq2d_factor(int m, int n, gptq2d_dtype dt, const void* A, int64_t lda,
+                            const void* B, int64_t ldb, void* stream, gptq2d_factors_t* out) {
+  if (!out) return fail(GPTQ2D_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  gptq2d_factors_t f = nullptr;
+  gptq2d_status st = gptq2d_factors_create(m, n, &f);
+  if (st != GPTQ2D_OK) return st;
+  st = gptq2d_factor_compute(f, dt, A, lda, B, ldb, stream);
+  if (st == GPTQ2D_OK) st = gptq2d_factor_check(f, stream);
+  if (st != GPTQ2D_OK) {
+    gptq2d_factors_destroy(f);
+    return st;
+  }
+  *out = f;
+  return GPTQ2D_OK;
+}
+
+gptq2d_status gptq2d_factors_export(gptq2d_factors_t f, double* L, int64_t ldl, double* U,
+                                    int64_t ldu, double* lamL, double* lamU, void* stream) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  if ((L && ldl < f->m) || (U && ldu < f->n))
+    return fail(GPTQ2D_ERR_INVALID_ARG, "leading dimension too small");
+  gptq2d_status st = check_device(f);
+  if (st != GPTQ2D_OK) return st;
+  return launch_export(*f, L, ldl, U, ldu, lamL, lamU, (hipStream_t)stream);
+}
+
+gptq2d_status gptq2d_factors_import(gptq2d_factors_t f, const double* L, int64_t ldl,
+                                    const double* U, int64_t ldu, const double* lamL,
+                                    const double* lamU, void* stream) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  if (!L || !U || !lamL || !lamU) return fail(GPTQ2D_ERR_INVALID_ARG, "a factor pointer is NULL");
+  if (ldl < f->m || ldu < f->n) return fail(GPTQ2D_ERR_INVALID_ARG, "leading dimension too small");
+  gptq2d_status st = check_device(f);
+  if (st != GPTQ2D_OK) return st;
+  return launch_import(*f, L, ldl, U, ldu, lamL, lamU, (hipStream_t)stream);
+}
+
+size_t gptq2d_round_workspace_size(gptq2d_factors_t f) { return f ? workspace_bytes(*f) : 0; }
+
+gptq2d_status gptq2d_round(gptq2d_factors_t f, gptq2d_dtype dt, const void* X, int64_t ldx,
+                           int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  if (dt != GPTQ2D_F32 && dt != GPTQ2D_F64) return fail(GPTQ2D_ERR_INVALID_ARG, "bad dtype");
+  if (!X || !Z) return fail(GPTQ2D_ERR_INVALID_ARG, "X or Z is NULL");
+  if (ldx < f->n || ldz < f->n || (Y && ldy < f->n))
+    return fail(GPTQ2D_ERR_INVALID_ARG, "leading dimension too small");
+  if (!workspace || ws_bytes < workspace_bytes(*f))
+    return fail(GPTQ2D_ERR_WORKSPACE, "workspace missing or smaller than gptq2d_round_workspace_size()");
+  if (((uintptr_t)workspace) % 256 != 0)
+    return fail(GPTQ2D_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  gptq2d_status st = check_device(f);
+  if (st != GPTQ2D_OK) return st;
+  Workspace ws = workspace_carve(*f, workspace);
+  return launch_round(*f, dt, X, ldx, Z, ldz, Y, ldy, objective, ws, (hipStream_t)stream);
+}
+
+gptq2d_status gptq2d_round_check(gptq2d_factors_t f, const void* workspace, void* stream) {
+  if (!f || !workspace) return fail(GPTQ2D_ERR_INVALID_ARG, "handle or workspace is NULL");
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  int flags = 0;
+  e = hipMemcpy(&flags, workspace, sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+  if (flags & FLAG_NONFINITE) return fail(GPTQ2D_ERR_NONFINITE, "X held a NaN or an infinity");
+  if (flags & FLAG_OVERFLOW) return fail(GPTQ2D_ERR_OVERFLOW, "a rounded value does not fit in int32");
+  return GPTQ2D_OK;
+}
+
+const char* gptq2d_status_string(gptq2d_status s) {
+  switch (s) {
+    case GPTQ2D_OK: return "ok";
+    case GPTQ2D_ERR_INVALID_ARG: return "invalid argument";
+    case GPTQ2D_ERR_SINGULAR: return "singular basis";
+    case GPTQ2D_ERR_NONFINITE: return "non-finite input";
+    case GPTQ2D_ERR_OOM: return "out of device memory";
+    case GPTQ2D_ERR_HIP: return "HIP runtime error";
+    case GPTQ2D_ERR_WORKSPACE: return "workspace missing or too small";
+    case GPTQ2D_ERR_OVERFLOW: return "rounded value outside int32";
+  }
+  return "unknown status";
+}
+
+const char* gptq2d_last_error(void) { return g_last_error.c_str(); }
+
+int gptq2d_version(void) { return 100; }
+
+int64_t gptq2d_schedule_tasks(int m, int n, int g, int32_t* tasks, int64_t cap, int32_t* offsets) {
+  if (m < 1 || n < 1 || m > 65536 || n > 65536 || g < 1) {
+    set_error("bad shape or batch width");
+    return -1;
+  }
+  const int MT = (m + TB - 1) / TB, NTt = (n + TB - 1) / TB;
+  std::vector<int4> all;
+  std::vector<int> off;
+  schedule_tasks(MT, NTt, g, all, off);
+  if (offsets)
+    for (size_t k = 0; k < off.size(); ++k) offsets[k] = off[k];
+  if (tasks) {
+    const int64_t nwrite = std::min<int64_t>(cap, (int64_t)all.size());
+    for (int64_t i = 0; i < nwrite; ++i) {
+      tasks[4 * i + 0] = all[i].x;
+      tasks[4 * i + 1] = all[i].y;
+      tasks[4 * i + 2] = all[i].z;
+      tasks[4 * i + 3] = all[i].w;
+    }
+  }
+  return (int64_t)all.size();
+}
+
+}  // extern "C"

@@ -1,0 +1,76 @@
+// Internal declarations of the GPTQ-2D library (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "gptq2d.h"
+
+namespace g2d {
+
+// Deferred-feedback delivery of the blocked sweep: one GEMM task that adds the
+// contribution of a contiguous run of finished source tiles to one target
+// tile. x = dir | overwrite << 1, y = target tile row, z = target tile
+// column, w = first source | (one past last source) << 16.
+struct Schedule {
+  int g = 0;                     // batch width in tile anti-diagonals
+  int stages = 0;                // tile anti-diagonals: MT + NT - 1
+  std::vector<int> offset;       // per stage: first task (size stages + 1)
+  int4* d_tasks = nullptr;       // all tasks, grouped by stage
+  size_t ntasks = 0;
+};
+
+struct Factors {
+  int m = 0, n = 0;     // problem shape
+  int mp = 0, np = 0;   // padded to multiples of 64
+  int MT = 0, NT = 0;   // tile counts
+  int device = 0;
+  // outputs of the factorisation (fp64, padded with an identity block)
+  double* L = nullptr;   // mp x mp, ld mp; unit lower; upper part not kept
+  double* U = nullptr;   // np x np, ld np; unit upper; lower part not kept
+  double* dL = nullptr;  // mp: 1 / lamL
+  double* dU = nullptr;  // np: 1 / lamU
+  // factorisation scratch, one set per side
+  double* gram[2] = {nullptr, nullptr};  // reversed Gram, then its Cholesky factor
+  double* inv[2] = {nullptr, nullptr};   // inverse of that Cholesky factor
+  double* dinv[2] = {nullptr, nullptr};  // inverses of its 64 x 64 diagonal blocks
+  int* flags = nullptr;                  // device error bits of the factorisation
+  Schedule sched;
+  std::vector<void*> allocations;
+};
+
+// workspace layout of gptq2d_round
+struct Workspace {
+  int* flags;
+  double* objp;  // per-tile objective partials, MT x NT
+  double* P;     // deferred down feedback (rows below), mp x np
+  double* R;     // deferred right feedback (columns to the left), mp x np
+  double* E;     // rounding errors, mp x np
+  double* C;     // the buffer C = L E, mp x np
+};
+size_t workspace_bytes(const Factors& f);
+Workspace workspace_carve(const Factors& f, void* base);
+
+// status plumbing
+void set_error(const std::string& msg);
+gptq2d_status hip_fail(hipError_t e, const char* what);
+
+// factorisation launches (enqueued on stream, no synchronisation)
+gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t lda,
+                            const void* B, int64_t ldb, hipStream_t s);
+gptq2d_status launch_export(const Factors& f, double* L, int64_t ldl, double* U, int64_t ldu,
+                            double* lamL, double* lamU, hipStream_t s);
+gptq2d_status launch_import(Factors& f, const double* L, int64_t ldl, const double* U,
+                            int64_t ldu, const double* lamL, const double* lamU, hipStream_t s);
+
+// sweep
+void schedule_tasks(int MT, int NT, int g, std::vector<int4>& all, std::vector<int>& offset);
+gptq2d_status build_schedule(Factors& f, int g);
+gptq2d_status launch_round(const Factors& f, gptq2d_dtype dt, const void* X, int64_t ldx,
+                           int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,
+                           const Workspace& ws, hipStream_t s);
+
+}  // namespace g2d

@@ -1,0 +1,150 @@
+"""GPU parity: the HIP path through the C ABI against the oracle.
+
+P1 -- the GPU factors against the oracle's (explicit inverse + LDL).
+P2 -- the GPU sweep, replayed by the oracle with the GPU's exported factors
+      (bit-identical factor data, no shared code).
+P3 -- end to end: the oracle's own factors.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_27042_amd import binding, workloads as wl
+
+import parity as pr
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(1, 1), (1, 100), (100, 1), (5, 7), (63, 65), (64, 64), (65, 64), (130, 200),
+          (200, 130), (256, 320)]
+
+
+def _factor_close(got, ref, tol):
+    err = np.abs(got - ref).max() / max(1.0, np.abs(ref).max())
+    assert err <= tol, err
+
+
+@pytest.mark.parametrize("m,n", [(1, 1), (5, 7), (63, 65), (130, 200), (256, 320)])
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_factors_match_oracle(m, n, dtype):
+    p = wl.random_problem(m, n, 1, dtype, "wishart")
+    res = pr.gpu_run(p)
+    X, A, B = p.widened()
+    L, lamL, U, lamU = oracle.factors(A, B)
+    _factor_close(res["L"], L, 1e-10)
+    _factor_close(res["U"], U, 1e-10)
+    np.testing.assert_allclose(res["lamL"], lamL, rtol=1e-10)
+    np.testing.assert_allclose(res["lamU"], lamU, rtol=1e-10)
+    assert np.array_equal(np.triu(res["L"], 1), np.zeros((m, m)))
+    assert np.array_equal(np.diag(res["L"]), np.ones(m))
+    assert np.array_equal(np.tril(res["U"], -1), np.zeros((n, n)))
+
+
+def test_factors_lower_triangular_closed_form():
+    """A lower => L = A^{-1} diag(A); B upper => U = diag(B) B^{-1}."""
+    import scipy.linalg as sla
+    p = wl.random_problem(150, 90, 2, "f64", "lower")
+    res = pr.gpu_run(p)
+    A, B = p.A, p.B
+    _factor_close(res["L"], sla.solve_triangular(A, np.diag(np.diag(A)), lower=True), 1e-11)
+    _factor_close(res["U"], np.diag(np.diag(B)) @ sla.solve_triangular(B, np.eye(90)), 1e-11)
+
+
+@pytest.mark.parametrize("m,n", SHAPES)
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_sweep_with_imported_factors(m, n, dtype):
+    """The sweep alone: oracle factors imported, replay with the same data."""
+    p = wl.random_problem(m, n, 4, dtype, "wishart")
+    X, A, B = p.widened()
+    fac = oracle.factors(A, B)
+    res = pr.gpu_run(p, factors=fac)
+    L, lamL, U, lamU = fac
+    Zo, Yo, c, hard = pr.replay(p, L, U, res["Z"])
+    pr.assert_replay_pass(p, c, hard, m * n)
+    tol = 1e-9 if dtype == "f64" else 2e-6 * max(1.0, np.abs(Yo).max())
+    assert np.abs(res["Y"] - Yo).max() <= tol
+    pr.assert_objective(p, res["obj"], oracle.objective(X, Zo, A, B))
+
+
+@pytest.mark.parametrize("m,n", SHAPES)
+@pytest.mark.parametrize("kind", ["wishart", "general"])
+def test_end_to_end(m, n, kind):
+    p = wl.random_problem(m, n, 5, "f64", kind)
+    X, A, B = p.widened()
+    res = pr.gpu_run(p)
+    # P2: replay under the GPU's own factors
+    Zo, Yo, c, hard = pr.replay(p, res["L"], res["U"], res["Z"])
+    pr.assert_replay_pass(p, c, hard, m * n)
+    assert np.abs(res["Y"] - Yo).max() <= 1e-9
+    # P3: the oracle's own factors
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zo3, Yo3, c3, hard3 = pr.replay(p, L, U, res["Z"])
+    pr.assert_replay_pass(p, c3, hard3, m * n)
+    pr.assert_objective(p, res["obj"], oracle.objective(X, Zo3, A, B))
+    pr.property_checks(p, res)
+
+
+@pytest.mark.parametrize("kind", ["diag", "identity_right", "identity_left", "lower"])
+def test_special_bases(kind):
+    p = wl.random_problem(97, 131, 6, "f64", kind)
+    X, A, B = p.widened()
+    res = pr.gpu_run(p)
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zo, Yo, c, hard = pr.replay(p, L, U, res["Z"])
+    pr.assert_replay_pass(p, c, hard, p.m * p.n)
+    if kind == "diag":
+        assert np.array_equal(res["Z"], np.rint(X).astype(np.int32))
+
+
+@pytest.mark.parametrize("k,dtype", [(1, "f64"), (2, "f32")])
+def test_small_configs(k, dtype):
+    p = wl.make_config(k, dtype)
+    X, A, B = p.widened()
+    res = pr.gpu_run(p)
+    Zo, Yo, c, hard = pr.replay(p, res["L"], res["U"], res["Z"])
+    pr.assert_replay_pass(p, c, hard, p.m * p.n)
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zo3, Yo3, c3, hard3 = pr.replay(p, L, U, res["Z"])
+    pr.assert_replay_pass(p, c3, hard3, p.m * p.n)
+    pr.assert_objective(p, res["obj"], oracle.objective(X, Zo3, A, B))
+
+
+def test_deterministic():
+    p = wl.random_problem(300, 260, 7, "f64", "wishart")
+    a = pr.gpu_run(p)
+    b = pr.gpu_run(p)
+    assert np.array_equal(a["Z"], b["Z"])
+    assert np.array_equal(a["Y"].view(np.int64), b["Y"].view(np.int64))
+    assert a["obj"] == b["obj"]
+
+
+def test_singular_basis_is_reported():
+    A = torch.zeros((70, 70), dtype=torch.float64, device="cuda")
+    B = torch.eye(40, dtype=torch.float64, device="cuda")
+    with pytest.raises(binding.Gptq2dError) as ei:
+        binding.Factors.from_bases(A, B)
+    assert ei.value.status == -2
+
+
+def test_nonfinite_input_is_reported():
+    p = wl.random_problem(80, 90, 8, "f64", "wishart")
+    f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B))
+    X = pr.to_dev(p.X)
+    X[10, 20] = float("nan")
+    with pytest.raises(binding.Gptq2dError) as ei:
+        binding.round_matrix(f, X)
+    assert ei.value.status == -3
+
+
+def test_argument_errors():
+    p = wl.random_problem(70, 50, 9, "f64", "wishart")
+    f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B))
+    X = pr.to_dev(p.X)
+    Z = torch.empty((70, 50), dtype=torch.int32, device="cuda")
+    small = torch.empty(128, dtype=torch.uint8, device="cuda")
+    with pytest.raises(binding.Gptq2dError) as ei:
+        binding.gptq2d_round(f.handle, X, Z, None, None, small)
+    assert ei.value.status == -6
+    with pytest.raises(ValueError):
+        binding.gptq2d_round(f.handle, X[:, :40], Z, None, None, f.workspace())
