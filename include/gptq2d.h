@@ -49,7 +49,8 @@ typedef enum {
   GPTQ2D_ERR_OOM = -4,         /* device allocation failed */
   GPTQ2D_ERR_HIP = -5,         /* a HIP runtime call failed */
   GPTQ2D_ERR_WORKSPACE = -6,   /* workspace missing or too small */
-  GPTQ2D_ERR_OVERFLOW = -7     /* a rounded value does not fit in int32 */
+  GPTQ2D_ERR_OVERFLOW = -7,    /* a rounded value does not fit in int32 */
+  GPTQ2D_ERR_TIMEOUT = -8      /* an internal wait between waves exceeded its bound */
 } gptq2d_status;
 
 /* ---------------------------------------------------------------------------
@@ -132,8 +133,8 @@ gptq2d_status gptq2d_round(gptq2d_factors_t f, gptq2d_dtype dt, const void* X, i
                            int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,
                            void* workspace, size_t ws_bytes, void* stream);
 
-/* Synchronises `stream` and returns NONFINITE or OVERFLOW if the last
- * gptq2d_round that used `workspace` met one, OK otherwise. */
+/* Synchronises `stream` and returns NONFINITE, OVERFLOW or TIMEOUT if the
+ * last gptq2d_round that used `workspace` met one, OK otherwise. */
 gptq2d_status gptq2d_round_check(gptq2d_factors_t f, const void* workspace, void* stream);
 
 /* ---------------------------------------------------------------------------

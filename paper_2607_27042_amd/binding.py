@@ -23,7 +23,7 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "gptq2d.h")
 
 F32, F64 = 0, 1
 STATUS = {0: "OK", -1: "ERR_INVALID_ARG", -2: "ERR_SINGULAR", -3: "ERR_NONFINITE", -4: "ERR_OOM",
-          -5: "ERR_HIP", -6: "ERR_WORKSPACE", -7: "ERR_OVERFLOW"}
+          -5: "ERR_HIP", -6: "ERR_WORKSPACE", -7: "ERR_OVERFLOW", -8: "ERR_TIMEOUT"}
 
 _lib = None
 

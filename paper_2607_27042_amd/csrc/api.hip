@@ -221,6 +221,7 @@ gptq2d_status gptq2d_round_check(gptq2d_factors_t f, const void* workspace, void
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
   if (flags & FLAG_NONFINITE) return fail(GPTQ2D_ERR_NONFINITE, "X held a NaN or an infinity");
   if (flags & FLAG_OVERFLOW) return fail(GPTQ2D_ERR_OVERFLOW, "a rounded value does not fit in int32");
+  if (flags & FLAG_TIMEOUT) return fail(GPTQ2D_ERR_TIMEOUT, "a wave waited too long for its neighbour");
   return GPTQ2D_OK;
 }
 
@@ -234,6 +235,7 @@ const char* gptq2d_status_string(gptq2d_status s) {
     case GPTQ2D_ERR_HIP: return "HIP runtime error";
     case GPTQ2D_ERR_WORKSPACE: return "workspace missing or too small";
     case GPTQ2D_ERR_OVERFLOW: return "rounded value outside int32";
+    case GPTQ2D_ERR_TIMEOUT: return "internal wait timed out";
   }
   return "unknown status";
 }

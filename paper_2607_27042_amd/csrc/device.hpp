@@ -160,7 +160,7 @@ __device__ __forceinline__ void acc_to_lds(const Acc& acc, double (*s)[LD]) {
 }
 
 // Device-scope error flags (bit set with a relaxed atomic OR).
-enum : int { FLAG_SINGULAR = 1, FLAG_NONFINITE = 2, FLAG_OVERFLOW = 4 };
+enum : int { FLAG_SINGULAR = 1, FLAG_NONFINITE = 2, FLAG_OVERFLOW = 4, FLAG_TIMEOUT = 8 };
 
 __device__ __forceinline__ void raise_flag(int* flags, int bit) {
   __hip_atomic_fetch_or(flags, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -92,57 +92,91 @@ __global__ __launch_bounds__(NT) void k_gram(const T* S, int64_t ld, int d, int 
 }
 
 // Cholesky of one 64 x 64 diagonal block (already updated by all previous
-// panels) and the inverse of the resulting lower factor, both in LDS. A pivot
-// that is not positive and finite raises FLAG_SINGULAR and is replaced by 1 so
-// that the remaining work stays finite.
+// panels) and the inverse of the resulting lower factor. Thread (c, g) with
+// c = t & 63, g = t >> 6 keeps rows g, g+4, .., g+60 of column c in registers;
+// each pivot step broadcasts one column through LDS (double-buffered, so two
+// barriers per step). A pivot that is not positive and finite raises
+// FLAG_SINGULAR and is replaced by 1 so that the remaining work stays finite.
 __global__ __launch_bounds__(NT) void k_potrf_diag(double* gr, int dp, int kb, double* dinv,
                                                    int* flags) {
   __shared__ double S[TB][TB + 1];
-  __shared__ double V[TB][TB + 1];
-  const int t = threadIdx.x;
+  __shared__ double col[2][TB];
+  const int t = threadIdx.x, c = t & 63, g = t >> 6;
   double* blk = gr + (int64_t)kb * TB * dp + (int64_t)kb * TB;
-  for (int e = t; e < TB * TB; e += NT) {
-    const int r = e >> 6, c = e & 63;
-    S[r][c] = blk[(int64_t)r * dp + c];
-    V[r][c] = (r == c) ? 1.0 : 0.0;
-  }
-  __syncthreads();
+  double a[16];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) a[u] = blk[(int64_t)(g + 4 * u) * dp + c];
   for (int j = 0; j < TB; ++j) {
-    if (t == 0) {
-      double piv = S[j][j];
-      if (!(piv > 0.0) || !isfinite(piv)) {
-        raise_flag(flags, FLAG_SINGULAR);
-        piv = 1.0;
+    double* cj = col[j & 1];
+    if (c == j) {
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        if (g + 4 * u == j) {
+          double piv = a[u];
+          if (!(piv > 0.0) || !isfinite(piv)) {
+            raise_flag(flags, FLAG_SINGULAR);
+            piv = 1.0;
+          }
+          a[u] = sqrt(piv);
+          cj[j] = a[u];
+        }
       }
-      S[j][j] = sqrt(piv);
     }
     __syncthreads();
-    const double ljj = S[j][j];
-    if (t > j && t < TB) S[t][j] /= ljj;
-    __syncthreads();
-    const int nt = TB - 1 - j;
-    for (int e = t; e < nt * nt; e += NT) {
-      const int i = j + 1 + e / nt, k = j + 1 + e % nt;
-      if (k <= i) S[i][k] -= S[i][j] * S[k][j];
+    if (c == j) {
+      const double inv = 1.0 / cj[j];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int i = g + 4 * u;
+        if (i > j) {
+          a[u] *= inv;
+          cj[i] = a[u];
+        }
+      }
     }
     __syncthreads();
+    if (c > j) {
+      const double cc = cj[c];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int i = g + 4 * u;
+        if (i >= c) a[u] -= cj[i] * cc;
+      }
+    }
   }
-  // V <- S^{-1}: forward substitution on the identity, one pivot row at a time
+#pragma unroll
+  for (int u = 0; u < 16; ++u) S[g + 4 * u][c] = a[u];
+  __syncthreads();
+  // v = S^{-1}, right-looking by pivot rows; thread (c, g) keeps rows g+4u of
+  // column c of the inverse (the pivot row is broadcast through a buffer that
+  // alternates with k, so one barrier per row suffices).
+  double v[16];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) v[u] = (g + 4 * u == c) ? 1.0 : 0.0;
   for (int k = 0; k < TB; ++k) {
-    if (t <= k) V[k][t] /= S[k][k];
-    __syncthreads();
-    const int w = k + 1, rows = TB - 1 - k;
-    for (int e = t; e < rows * w; e += NT) {
-      const int i = k + 1 + e / w, c = e % w;
-      V[i][c] -= S[i][k] * V[k][c];
+    double* rk = col[k & 1];
+    if ((k & 3) == g) {
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (4 * u + g == k) {
+          v[u] = v[u] / S[k][k];
+          rk[c] = v[u];
+        }
     }
     __syncthreads();
+    const double x = rk[c];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int i = g + 4 * u;
+      if (i > k) v[u] -= S[i][k] * x;
+    }
   }
   double* dv = dinv + (int64_t)kb * TB * TB;
-  for (int e = t; e < TB * TB; e += NT) {
-    const int r = e >> 6, c = e & 63;
-    blk[(int64_t)r * dp + c] = (c <= r) ? S[r][c] : 0.0;
-    dv[e] = (c <= r) ? V[r][c] : 0.0;
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int i = g + 4 * u;
+    blk[(int64_t)i * dp + c] = (c <= i) ? a[u] : 0.0;
+    dv[i * TB + c] = (c <= i) ? v[u] : 0.0;
   }
 }
 

@@ -53,207 +53,419 @@ struct StageArgs {
   int stage, ilo, nsweep;
 };
 
+// A whole 64-deep contraction block of both operands, k-major.
+constexpr int GSA = TB + 1;  // odd stride: transposed writes spread over the banks
+constexpr int GSB = TB + 2;
+struct Stage64 {
+  double a[TB][GSA];  // a[k][i] = A[i][k]
+  double b[TB][GSB];  // b[k][j] = B[k][j]
+};
+
+constexpr int SS = 16;       // sub-tile edge of the in-tile sweep
+constexpr int TP = TB + 2;   // LDS row stride of the tile arrays (doubles)
+
+// LDS of a sweeping workgroup. Ls, Us: the diagonal factor blocks L_II and
+// U_JJ with a zero column 64 (Ls) and a zero row 64 (Us) for out-of-block
+// window indices. Et, Ct: the tile's E and C as its sub-tiles finish (the
+// operands of the in-tile feedback products); before the sweep the same bytes
+// stage the two neighbour products.
 struct SweepSmem {
-  double LsT[TB + 1][TB];     // LsT[x][r] = L_II[r][x]; row 64 is zero
-  double Us[TB + 1][TB + 2];  // Us[y][k] = U_JJ[y][k]; row 64 is zero
-  double ev[2][TB];           // error of the active entry of column k
-  double cv[2][TB];           // C value of the active entry of row r
+  double Ls[TB][TP];
+  double Us[TB + 1][TP];
   union {
+    struct {
+      double Et[TB][TP];
+      double Ct[TB][TP];
+    } t;
+    Stage64 g;
     double T[TB][TB + 1];
-    GemmSmem g;
   } x;
-  double red[NT];
+  double xe[4][SS];          // per wave: error of the active entry of each sub-tile column
+  double xc[4][SS];          // per wave: C value of the active entry of each sub-tile row
+  double scr[4][SS][SS + 1]; // per wave: MFMA-layout to block-layout transfer
+  double red[NT / 64];
+  int done[4];               // per wave: sub-tiles finished (release/acquire, workgroup scope)
+};
+
+struct TaskSmem {
+  Stage64 buf[2];
 };
 
 union StageSmem {
   SweepSmem s;
-  GemmSmem g;
+  TaskSmem t;
 };
+
+// 64 x 64 fp64 block at p (row-major, ld) into registers: element
+// (e >> 6, e & 63) with e = threadIdx.x + 256 s goes to r[s] (coalesced).
+__device__ __forceinline__ void load_blk(const double* p, int64_t ld, double r[16]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s;
+    r[s] = p[(int64_t)(e >> 6) * ld + (e & 63)];
+  }
+}
+// left operand A[i][k] = r -> a[k][i]
+__device__ __forceinline__ void put_a(Stage64& st, const double r[16]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s;
+    st.a[e & 63][e >> 6] = r[s];
+  }
+}
+// right operand B[k][j] = r -> b[k][j]
+__device__ __forceinline__ void put_b(Stage64& st, const double r[16]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s;
+    st.b[e >> 6][e & 63] = r[s];
+  }
+}
+// acc += (staged A) (staged B) over the 64-deep block.
+__device__ __forceinline__ void mma_blk(Acc& acc, const Stage64& st) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int rb = 32 * (w >> 1) + (l & 15), cb = 32 * (w & 1) + (l & 15);
+#pragma unroll
+  for (int kk = 0; kk < TB / 4; ++kk) {
+    const int k = 4 * kk + (l >> 4);
+    const double a0 = st.a[k][rb], a1 = st.a[k][rb + 16];
+    const double b0 = st.b[k][cb], b1 = st.b[k][cb + 16];
+    acc.t[0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc.t[0], 0, 0, 0);
+    acc.t[1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc.t[1], 0, 0, 0);
+    acc.t[2] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc.t[2], 0, 0, 0);
+    acc.t[3] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc.t[3], 0, 0, 0);
+  }
+}
 
 template <typename T>
 __device__ __forceinline__ double load_x(const T* X, int64_t ldx, int gi, int gj, int m, int n) {
   return (gi < m && gj < n) ? (double)X[(int64_t)gi * ldx + gj] : 0.0;
 }
 
-// One deferred-feedback delivery (a GEMM task).
-__device__ void run_task(const StageArgs& a, int4 tk, GemmSmem& sm) {
+// One deferred-feedback delivery (a GEMM task), 64-deep blocks double-buffered
+// through LDS: the loads of block b+1 are in flight while block b is on MFMA.
+__device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
   const int dir = tk.x & 1, ow = (tk.x >> 1) & 1;
   const int ti = tk.y, tj = tk.z, s0 = tk.w & 0xffff, s1 = tk.w >> 16;
-  const int K = (s1 - s0) * TB;
-  Acc acc;
-  acc.zero();
+  const double* Ap;
+  const double* Bp;
+  int64_t lda;
   double* out;
   if (dir == 0) {
-    gemm_acc(acc, OpRK{a.L + (int64_t)ti * TB * a.mp + (int64_t)s0 * TB, a.mp},
-             OpKR{a.E + (int64_t)s0 * TB * a.np + (int64_t)tj * TB, a.np}, K, sm);
+    Ap = a.L + (int64_t)ti * TB * a.mp + (int64_t)s0 * TB;
+    lda = a.mp;
+    Bp = a.E + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
     out = a.P + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
   } else {
-    gemm_acc(acc, OpRK{a.C + (int64_t)ti * TB * a.np + (int64_t)s0 * TB, a.np},
-             OpKR{a.U + (int64_t)s0 * TB * a.np + (int64_t)tj * TB, a.np}, K, sm);
+    Ap = a.C + (int64_t)ti * TB * a.np + (int64_t)s0 * TB;
+    lda = a.np;
+    Bp = a.U + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
     out = a.R + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
   }
+  const int64_t ldb = a.np;
+  Acc acc;
+  acc.zero();
   if (!ow) acc_add_from(acc, out, a.np);
+  double ra[16], rb[16];
+  load_blk(Ap, lda, ra);
+  load_blk(Bp, ldb, rb);
+  const int nb = s1 - s0;
+  for (int b = 0; b < nb; ++b) {
+    Stage64& st = sm.buf[b & 1];
+    put_a(st, ra);
+    put_b(st, rb);
+    __syncthreads();
+    if (b + 1 < nb) {
+      load_blk(Ap + (int64_t)(b + 1) * TB, lda, ra);
+      load_blk(Bp + (int64_t)(b + 1) * TB * ldb, ldb, rb);
+    }
+    mma_blk(acc, st);
+  }
   acc_store(acc, out, a.np, 1.0);
 }
 
-// Sweep of one tile. Thread layout: wave w, lane l; q = 4w + (l >> 4) picks
-// columns 4q .. 4q+3 and p = l & 15 rows 4p .. 4p+3; each thread keeps its
-// 4 x 4 block of the tile in registers.
+// acc += A (16 x K) B (K x 16) on MFMA, both operands in LDS, row-major with
+// row strides lda, ldb; K a multiple of 4 (0 allowed). One wave.
+// K <= 48; every operand load is issued before the first MFMA.
+__device__ __forceinline__ void mma16(d4& acc, const double* pa, int lda, const double* pb, int ldb,
+                                      int K) {
+  const int l = threadIdx.x & 63;
+  double av[12], bv[12];
+#pragma unroll
+  for (int s = 0; s < 12; ++s) {
+    if (4 * s < K) {
+      av[s] = pa[(l & 15) * lda + 4 * s + (l >> 4)];
+      bv[s] = pb[(4 * s + (l >> 4)) * ldb + (l & 15)];
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < 12; ++s)
+    if (4 * s < K) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[s], bv[s], acc, 0, 0, 0);
+}
+
+// Sweep of one tile. Wave w owns the 16-row band 16w .. 16w+15 and sweeps its
+// four 16 x 16 sub-tiles left to right, one wave per sub-tile, so that the
+// per-anti-diagonal exchange stays inside the wave (LDS, no workgroup
+// barrier). Sub-tile (w, c) starts when the band above has finished
+// sub-tile c; the feedback from the finished sub-tiles above and to the left
+// is added first as two small MFMA products. Lane l owns the 2 x 2 block at
+// band rows 2p, 2p+1 (p = l & 7) and sub-tile columns 2q, 2q+1 (q = l >> 3).
 template <typename T>
 __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
-  const int t = threadIdx.x;
-  const int q = 4 * (t >> 6) + ((t & 63) >> 4);
-  const int p = t & 15;
-  const int r0 = 4 * p, k0 = 4 * q;
+  const int t = threadIdx.x, w = t >> 6, l = t & 63;
+  const int p = l & 7, q = l >> 3;
+  const int br = SS * w + 2 * p;  // tile row of the lane's first row
   const int gi0 = I * TB, gj0 = J * TB;
+  const T* X = (const T*)a.X;
 
-  // diagonal factor blocks into LDS; zero rows for out-of-tile indices
-  for (int e = t; e < TB * TB; e += NT) {
-    const int r = e >> 6, x = e & 63;
-    sm.LsT[x][r] = a.L[(int64_t)(gi0 + r) * a.mp + gi0 + x];
-    sm.Us[r][x] = a.U[(int64_t)(gj0 + r) * a.np + gj0 + x];
+  // every global load of the prologue is issued before any is used
+  double lv[16], uv[16], ga[16], gb[16];
+  load_blk(a.L + (int64_t)gi0 * a.mp + gi0, a.mp, lv);
+  load_blk(a.U + (int64_t)gj0 * a.np + gj0, a.np, uv);
+  if (I >= 1) {
+    load_blk(a.L + (int64_t)gi0 * a.mp + (gi0 - TB), a.mp, ga);
+    load_blk(a.E + (int64_t)(gi0 - TB) * a.np + gj0, a.np, gb);
+  }
+  double Dn[4][2][2], Rt[4][2][2], dl[2], du[4][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) dl[i] = a.dL[gi0 + br + i];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) du[c][j] = a.dU[gj0 + SS * c + 2 * q + j];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int gi = gi0 + br + i, gj = gj0 + SS * c + 2 * q + j;
+        double r = load_x<T>(X, a.ldx, gi, gj, a.m, a.n);
+        if (J >= 2) r += a.R[(int64_t)gi * a.np + gj];
+        Rt[c][i][j] = r;
+        Dn[c][i][j] = (I >= 2) ? a.P[(int64_t)gi * a.np + gj] : 0.0;
+      }
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s, r = e >> 6, x = e & 63;
+    sm.Ls[r][x] = lv[s];
+    sm.Us[r][x] = uv[s];
   }
   if (t < TB) {
-    sm.LsT[TB][t] = 0.0;
+    sm.Ls[t][TB] = 0.0;
     sm.Us[TB][t] = 0.0;
-    sm.ev[0][t] = sm.ev[1][t] = 0.0;
-    sm.cv[0][t] = sm.cv[1][t] = 0.0;
   }
+  if (t < 4 * SS) {
+    sm.xe[t >> 4][t & 15] = 0.0;
+    sm.xc[t >> 4][t & 15] = 0.0;
+  }
+  if (t < 4) sm.done[t] = 0;
 
-  double Dn[4][4], Rt[4][4];
-  // down feedback: P (older tiles above) + L[I][I-1] E[I-1][J]
-  {
-    Acc acc;
+  // feedback of the neighbouring tiles: L[I][I-1] E[I-1][J] and C[I][J-1] U[J-1][J]
+  Acc acc;
+  if (I >= 1) {
     acc.zero();
-    if (I >= 1)
-      gemm_acc(acc, OpRK{a.L + (int64_t)gi0 * a.mp + (int64_t)(gi0 - TB), a.mp},
-               OpKR{a.E + (int64_t)(gi0 - TB) * a.np + gj0, a.np}, TB, sm.x.g);
-    if (I >= 2) acc_add_from(acc, a.P + (int64_t)gi0 * a.np + gj0, a.np);
+    put_a(sm.x.g, ga);
+    put_b(sm.x.g, gb);
+    __syncthreads();
+    mma_blk(acc, sm.x.g);
+  }
+  if (J >= 1) {  // operands of the right product, in flight during the above
+    load_blk(a.C + (int64_t)gi0 * a.np + (gj0 - TB), a.np, ga);
+    load_blk(a.U + (int64_t)(gj0 - TB) * a.np + gj0, a.np, gb);
+  }
+  if (I >= 1) {
+    __syncthreads();
     acc_to_lds<TB + 1>(acc, sm.x.T);
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int c = 0; c < 4; ++c)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) Dn[i][j] = sm.x.T[r0 + i][k0 + j];
-    __syncthreads();
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) Dn[c][i][j] += sm.x.T[br + i][SS * c + 2 * q + j];
   }
-  // right feedback: R (older tiles to the left) + C[I][J-1] U[J-1][J], plus X
-  {
-    Acc acc;
+  if (J >= 1) {
     acc.zero();
-    if (J >= 1)
-      gemm_acc(acc, OpRK{a.C + (int64_t)gi0 * a.np + (int64_t)(gj0 - TB), a.np},
-               OpKR{a.U + (int64_t)(gj0 - TB) * a.np + gj0, a.np}, TB, sm.x.g);
-    if (J >= 2) acc_add_from(acc, a.R + (int64_t)gi0 * a.np + gj0, a.np);
+    __syncthreads();
+    put_a(sm.x.g, ga);
+    put_b(sm.x.g, gb);
+    __syncthreads();
+    mma_blk(acc, sm.x.g);
+    __syncthreads();
     acc_to_lds<TB + 1>(acc, sm.x.T);
     __syncthreads();
-    const T* X = (const T*)a.X;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int c = 0; c < 4; ++c)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        Rt[i][j] = sm.x.T[r0 + i][k0 + j] + load_x<T>(X, a.ldx, gi0 + r0 + i, gj0 + k0 + j, a.m, a.n);
-    __syncthreads();
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) Rt[c][i][j] += sm.x.T[br + i][SS * c + 2 * q + j];
   }
+  __syncthreads();
 
-  // In-tile Algorithm 3. Stage d handles the entries with r + k == d. The
-  // window Lw[x & 3][i] holds L[r0+i][x] for x = d-k0-3 .. d-k0 and
-  // Uw[y & 3][j] holds U[y][k0+j] for y = d-r0-3 .. d-r0.
-  double yf[4][4], cf[4][4], Lw[4][4], Uw[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      Lw[i][j] = 0.0;
-      Uw[i][j] = 0.0;
-      yf[i][j] = 0.0;
-      cf[i][j] = 0.0;
-    }
-  const int pq = p + q;
-  for (int D = 0; D < TB / 2; ++D) {
-#pragma unroll
-    for (int dl = 0; dl < 4; ++dl) {
-      const int d = 4 * D + dl;
-      if (d <= 2 * TB - 2) {
-        int x = d - k0;
-        x = (x < 0 || x >= TB) ? TB : x;
-        int y = d - r0;
-        y = (y < 0 || y >= TB) ? TB : y;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) Lw[dl][i] = sm.LsT[x][r0 + i];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) Uw[dl][j] = sm.Us[y][k0 + j];
-        const int buf = dl & 1;
-        // round the entries of this thread's block that lie on anti-diagonal d
-#pragma unroll
-        for (int grp = 0; grp < 2; ++grp) {
-          if (D == pq + grp) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int j = dl + 4 * grp - i;
-              if (j >= 0 && j < 4) {
-                const double yv = Rt[i][j] + Dn[i][j];
-                const double z = rint(yv);
-                const double e = z - yv;
-                const double c = Dn[i][j] + e;
-                yf[i][j] = yv;
-                cf[i][j] = c;
-                sm.ev[buf][k0 + j] = e;
-                sm.cv[buf][r0 + i] = c;
-              }
-            }
-          }
-        }
-        __syncthreads();
-        double e4[4], c4[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) e4[j] = sm.ev[buf][k0 + j];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) c4[i] = sm.cv[buf][r0 + i];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            Dn[i][j] += Lw[(dl - j) & 3][i] * e4[j];  // push down
-            Rt[i][j] += c4[i] * Uw[(dl - i) & 3][j];  // push right
-          }
-      }
-    }
-  }
-
-  // outputs
   double part = 0.0;
   int bad = 0;
   T* Y = (T*)a.Y;
+  const int pq2 = 2 * (p + q);
+#pragma unroll 1
+  for (int c = 0; c < 4; ++c) {
+    // this sub-tile's share of the band state (kept rolled: small code)
+    double Dc[2][2], Rc[2][2], dc[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int gi = gi0 + r0 + i;
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int gj = gj0 + k0 + j;
-      const double yv = yf[i][j];
-      const double z = rint(yv);
-      const double e = z - yv;
-      a.E[(int64_t)gi * a.np + gj] = e;
-      a.C[(int64_t)gi * a.np + gj] = cf[i][j];
-      if (gi < a.m && gj < a.n) {
-        if (!isfinite(yv)) bad |= FLAG_NONFINITE;
-        else if (fabs(z) > 2147483647.0) bad |= FLAG_OVERFLOW;
-        const double zc = fmin(fmax(z, -2147483648.0), 2147483647.0);
-        a.Z[(int64_t)gi * a.ldz + gj] = isfinite(zc) ? (int32_t)zc : 0;
-        if (Y) Y[(int64_t)gi * a.ldy + gj] = (T)yv;
-        part += e * e * a.dL[gi] * a.dU[gj];
+      for (int j = 0; j < 2; ++j) {
+        Dc[i][j] = c == 0 ? Dn[0][i][j] : c == 1 ? Dn[1][i][j] : c == 2 ? Dn[2][i][j] : Dn[3][i][j];
+        Rc[i][j] = c == 0 ? Rt[0][i][j] : c == 1 ? Rt[1][i][j] : c == 2 ? Rt[2][i][j] : Rt[3][i][j];
+      }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) dc[j] = c == 0 ? du[0][j] : c == 1 ? du[1][j] : c == 2 ? du[2][j] : du[3][j];
+    // the band above must have finished sub-tile c
+    if (w > 0) {
+      int spins = 0;
+      while (__hip_atomic_load(&sm.done[w - 1], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) <= c) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++spins > (1 << 22)) {
+          bad |= FLAG_TIMEOUT;
+          break;
+        }
+      }
+    }
+    // feedback from the finished sub-tiles above (same column) and to the
+    // left (same band) inside this tile
+    {
+      d4 aD = {0.0, 0.0, 0.0, 0.0}, aR = {0.0, 0.0, 0.0, 0.0};
+      mma16(aD, &sm.Ls[SS * w][0], TP, &sm.x.t.Et[0][SS * c], TP, SS * w);
+      mma16(aR, &sm.x.t.Ct[SS * w][0], TP, &sm.Us[0][SS * c], TP, SS * c);
+      double(*sc)[SS + 1] = sm.scr[w];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sc[4 * r + (l >> 4)][l & 15] = aD[r];
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) Dc[i][j] += sc[2 * p + i][2 * q + j];
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sc[4 * r + (l >> 4)][l & 15] = aR[r];
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) Rc[i][j] += sc[2 * p + i][2 * q + j];
+      __builtin_amdgcn_wave_barrier();
+    }
+
+    // Algorithm 3 on the 16 x 16 sub-tile. Iteration d applies the pushes of
+    // anti-diagonal d-1 and rounds the entries on anti-diagonal d; the two
+    // pushes that complete an entry about to be rounded are applied first.
+    // Window slot (x & 1) of Lw holds L[br+i][16w+x], slot (y & 1) of Uw holds
+    // U[16c+y][16c+2q+j]; the entries of anti-diagonal d are loaded in
+    // iteration d and committed after its pushes.
+    const int lr = SS * w, uc = SS * c;
+    double Lw[2][2] = {{0.0, 0.0}, {0.0, 0.0}}, Uw[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
+    double yf[2][2] = {{0.0, 0.0}, {0.0, 0.0}}, cf[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
+    double* xe = sm.xe[w];
+    double* xc = sm.xc[w];
+#pragma unroll 1
+    for (int D2 = 0; D2 < SS; ++D2) {
+#pragma unroll
+      for (int dd = 0; dd < 2; ++dd) {
+        const int d = 2 * D2 + dd;
+        if (d <= 2 * SS - 2) {
+          const int ps = dd ^ 1;  // window slot of anti-diagonal d-1
+          const double e0 = xe[2 * q], e1 = xe[2 * q + 1];
+          const double c0 = xc[2 * p], c1 = xc[2 * p + 1];
+          const double e2[2] = {e0, e1}, c2[2] = {c0, c1};
+          const int x = d - 2 * q, y = d - 2 * p;
+          const int xi = (x >= 0 && x < SS) ? lr + x : TB;
+          const int yi = (y >= 0 && y < SS) ? uc + y : TB;
+          const double Ln[2] = {sm.Ls[br][xi], sm.Ls[br + 1][xi]};
+          const double Un[2] = {sm.Us[yi][uc + 2 * q], sm.Us[yi][uc + 2 * q + 1]};
+#define G2D_ROUND(I_, J_)                                                        \
+  {                                                                              \
+    const double dn = Dc[I_][J_] + Lw[(ps - (J_)) & 1][I_] * e2[J_];          \
+    const double rt = Rc[I_][J_] + c2[I_] * Uw[(ps - (I_)) & 1][J_];          \
+    const double yv = rt + dn;                                                   \
+    const double z = rint(yv);                                                   \
+    const double ev = z - yv;                                                    \
+    const double cv = dn + ev;                                                   \
+    yf[I_][J_] = yv;                                                             \
+    cf[I_][J_] = cv;                                                             \
+    xe[2 * q + (J_)] = ev;                                                       \
+    xc[2 * p + (I_)] = cv;                                                       \
+  }
+          if (dd == 0) {
+            if (d == pq2) G2D_ROUND(0, 0)
+            if (d == pq2 + 2) G2D_ROUND(1, 1)
+          } else {
+            if (d == pq2 + 1) {
+              G2D_ROUND(0, 1)
+              G2D_ROUND(1, 0)
+            }
+          }
+#undef G2D_ROUND
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+              Dc[i][j] += Lw[(ps - j) & 1][i] * e2[j];  // push down
+              Rc[i][j] += c2[i] * Uw[(ps - i) & 1][j];  // push right
+            }
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            Lw[dd][i] = Ln[i];
+            Uw[dd][i] = Un[i];
+          }
+          __builtin_amdgcn_wave_barrier();
+        }
+      }
+    }
+
+    // results of sub-tile (w, c): E and C into LDS for the sub-tiles below
+    // and to the right, then the hand-off, then the global outputs
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const double yv = yf[i][j];
+        sm.x.t.Et[br + i][SS * c + 2 * q + j] = rint(yv) - yv;
+        sm.x.t.Ct[br + i][SS * c + 2 * q + j] = cf[i][j];
+      }
+    __hip_atomic_store(&sm.done[w], c + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int gi = gi0 + br + i;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int gj = gj0 + SS * c + 2 * q + j;
+        const double yv = yf[i][j];
+        const double z = rint(yv);
+        const double e = z - yv;
+        a.E[(int64_t)gi * a.np + gj] = e;
+        a.C[(int64_t)gi * a.np + gj] = cf[i][j];
+        if (gi < a.m && gj < a.n) {
+          if (!isfinite(yv)) bad |= FLAG_NONFINITE;
+          else if (fabs(z) > 2147483647.0) bad |= FLAG_OVERFLOW;
+          const double zc = fmin(fmax(z, -2147483648.0), 2147483647.0);
+          a.Z[(int64_t)gi * a.ldz + gj] = isfinite(zc) ? (int32_t)zc : 0;
+          if (Y) Y[(int64_t)gi * a.ldy + gj] = (T)yv;
+          part += e * e * dl[i] * dc[j];
+        }
       }
     }
   }
+
   if (bad) raise_flag(a.flags, bad);
-  sm.red[t] = part;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
+  if (l == 0) sm.red[w] = part;
   __syncthreads();
-  if (t == 0) {
-    double s = 0.0;
-    for (int i = 0; i < NT; ++i) s += sm.red[i];
-    a.objp[I * a.NT + J] = s;
-  }
+  if (t == 0) a.objp[I * a.NT + J] = (sm.red[0] + sm.red[1]) + (sm.red[2] + sm.red[3]);
 }
 
 template <typename T>
@@ -264,7 +476,7 @@ __global__ __launch_bounds__(NT) void k_stage(StageArgs a) {
     const int I = a.ilo + b;
     run_sweep<T>(a, I, a.stage - I, sm.s);
   } else {
-    run_task(a, a.tasks[b - a.nsweep], sm.g);
+    run_task(a, a.tasks[b - a.nsweep], sm.t);
   }
 }
 
