@@ -159,6 +159,75 @@ __device__ __forceinline__ void acc_to_lds(const Acc& acc, double (*s)[LD]) {
       for (int r = 0; r < 4; ++r) s[acc_row(u, r)][acc_col(v)] = acc.t[2 * u + v][r];
 }
 
+
+// ---------------------------------------------------------------------------
+// Whole-block staging: both operands of a 64-deep contraction are loaded into
+// registers at once (one memory latency), written k-major into LDS and
+// consumed by 64 MFMA k-steps per wave.
+// ---------------------------------------------------------------------------
+
+// A whole 64-deep contraction block of both operands, k-major.
+constexpr int GSA = TB + 1;  // odd stride: transposed writes spread over the banks
+constexpr int GSB = TB + 2;
+struct Stage64 {
+  double a[TB][GSA];  // a[k][i] = A[i][k]
+  double b[TB][GSB];  // b[k][j] = B[k][j]
+};
+
+// 64 x 64 fp64 block at p (row-major, ld) into registers: element
+// (e >> 6, e & 63) with e = threadIdx.x + 256 s goes to r[s] (coalesced).
+__device__ __forceinline__ void load_blk(const double* p, int64_t ld, double r[16]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s;
+    r[s] = p[(int64_t)(e >> 6) * ld + (e & 63)];
+  }
+}
+// left operand A[i][k] = r -> a[k][i]
+__device__ __forceinline__ void put_a(Stage64& st, const double r[16]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s;
+    st.a[e & 63][e >> 6] = r[s];
+  }
+}
+// right operand B[k][j] = r -> b[k][j]
+__device__ __forceinline__ void put_b(Stage64& st, const double r[16]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s;
+    st.b[e >> 6][e & 63] = r[s];
+  }
+}
+// acc += (staged A) (staged B) over the 64-deep block.
+__device__ __forceinline__ void mma_blk(Acc& acc, const Stage64& st) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int rb = 32 * (w >> 1) + (l & 15), cb = 32 * (w & 1) + (l & 15);
+#pragma unroll
+  for (int kk = 0; kk < TB / 4; ++kk) {
+    const int k = 4 * kk + (l >> 4);
+    const double a0 = st.a[k][rb], a1 = st.a[k][rb + 16];
+    const double b0 = st.b[k][cb], b1 = st.b[k][cb + 16];
+    acc.t[0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc.t[0], 0, 0, 0);
+    acc.t[1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc.t[1], 0, 0, 0);
+    acc.t[2] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc.t[2], 0, 0, 0);
+    acc.t[3] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc.t[3], 0, 0, 0);
+  }
+}
+
+// right operand given transposed, B^T[j][k] = r -> b[k][j]
+__device__ __forceinline__ void put_bt(Stage64& st, const double r[16]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s;
+    st.b[e & 63][e >> 6] = r[s];
+  }
+}
+
 // Device-scope error flags (bit set with a relaxed atomic OR).
 enum : int { FLAG_SINGULAR = 1, FLAG_NONFINITE = 2, FLAG_OVERFLOW = 4, FLAG_TIMEOUT = 8 };
 

@@ -53,14 +53,6 @@ struct StageArgs {
   int stage, ilo, nsweep;
 };
 
-// A whole 64-deep contraction block of both operands, k-major.
-constexpr int GSA = TB + 1;  // odd stride: transposed writes spread over the banks
-constexpr int GSB = TB + 2;
-struct Stage64 {
-  double a[TB][GSA];  // a[k][i] = A[i][k]
-  double b[TB][GSB];  // b[k][j] = B[k][j]
-};
-
 constexpr int SS = 16;       // sub-tile edge of the in-tile sweep
 constexpr int TP = TB + 2;   // LDS row stride of the tile arrays (doubles)
 
@@ -96,53 +88,13 @@ union StageSmem {
   TaskSmem t;
 };
 
-// 64 x 64 fp64 block at p (row-major, ld) into registers: element
-// (e >> 6, e & 63) with e = threadIdx.x + 256 s goes to r[s] (coalesced).
-__device__ __forceinline__ void load_blk(const double* p, int64_t ld, double r[16]) {
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int s = 0; s < 16; ++s) {
-    const int e = t + NT * s;
-    r[s] = p[(int64_t)(e >> 6) * ld + (e & 63)];
-  }
-}
-// left operand A[i][k] = r -> a[k][i]
-__device__ __forceinline__ void put_a(Stage64& st, const double r[16]) {
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int s = 0; s < 16; ++s) {
-    const int e = t + NT * s;
-    st.a[e & 63][e >> 6] = r[s];
-  }
-}
-// right operand B[k][j] = r -> b[k][j]
-__device__ __forceinline__ void put_b(Stage64& st, const double r[16]) {
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int s = 0; s < 16; ++s) {
-    const int e = t + NT * s;
-    st.b[e >> 6][e & 63] = r[s];
-  }
-}
-// acc += (staged A) (staged B) over the 64-deep block.
-__device__ __forceinline__ void mma_blk(Acc& acc, const Stage64& st) {
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const int rb = 32 * (w >> 1) + (l & 15), cb = 32 * (w & 1) + (l & 15);
-#pragma unroll
-  for (int kk = 0; kk < TB / 4; ++kk) {
-    const int k = 4 * kk + (l >> 4);
-    const double a0 = st.a[k][rb], a1 = st.a[k][rb + 16];
-    const double b0 = st.b[k][cb], b1 = st.b[k][cb + 16];
-    acc.t[0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc.t[0], 0, 0, 0);
-    acc.t[1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc.t[1], 0, 0, 0);
-    acc.t[2] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc.t[2], 0, 0, 0);
-    acc.t[3] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc.t[3], 0, 0, 0);
-  }
-}
-
+// X[gi][gj] widened, 0 outside the matrix; the load is unconditional (from a
+// clamped address) so that it does not serialise behind a branch.
 template <typename T>
 __device__ __forceinline__ double load_x(const T* X, int64_t ldx, int gi, int gj, int m, int n) {
-  return (gi < m && gj < n) ? (double)X[(int64_t)gi * ldx + gj] : 0.0;
+  const bool ok = gi < m && gj < n;
+  const T v = X[ok ? (int64_t)gi * ldx + gj : 0];
+  return ok ? (double)v : 0.0;
 }
 
 // One deferred-feedback delivery (a GEMM task), 64-deep blocks double-buffered
