@@ -57,13 +57,13 @@ constexpr int SS = 16;       // sub-tile edge of the in-tile sweep
 constexpr int TP = TB + 2;   // LDS row stride of the tile arrays (doubles)
 
 // LDS of a sweeping workgroup. Ls, Us: the diagonal factor blocks L_II and
-// U_JJ with a zero column 64 (Ls) and a zero row 64 (Us) for out-of-block
-// window indices. Et, Ct: the tile's E and C as its sub-tiles finish (the
+// U_JJ with zero columns 64, 65 (Ls) and zero rows 64, 65 (Us) for source
+// blocks that do not exist. Et, Ct: the tile's E and C as its sub-tiles finish (the
 // operands of the in-tile feedback products); before the sweep the same bytes
 // stage the two neighbour products.
 struct SweepSmem {
   double Ls[TB][TP];
-  double Us[TB + 1][TP];
+  double Us[TB + 2][TP];
   union {
     struct {
       double Et[TB][TP];
@@ -72,8 +72,6 @@ struct SweepSmem {
     Stage64 g;
     double T[TB][TB + 1];
   } x;
-  double xe[4][SS];          // per wave: error of the active entry of each sub-tile column
-  double xc[4][SS];          // per wave: C value of the active entry of each sub-tile row
   double scr[4][SS][SS + 1]; // per wave: MFMA-layout to block-layout transfer
   double red[NT / 64];
   int done[4];               // per wave: sub-tiles finished (release/acquire, workgroup scope)
@@ -139,23 +137,181 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
   acc_store(acc, out, a.np, 1.0);
 }
 
-// acc += A (16 x K) B (K x 16) on MFMA, both operands in LDS, row-major with
-// row strides lda, ldb; K a multiple of 4 (0 allowed). One wave.
-// K <= 48; every operand load is issued before the first MFMA.
+// acc += A (16 x K) B (K x 16) on MFMA, both operands row-major in LDS with
+// row strides lda, ldb; K a multiple of 16 (0 allowed). One wave. Each
+// 16-deep chunk issues its eight operand loads before its four MFMAs.
 __device__ __forceinline__ void mma16(d4& acc, const double* pa, int lda, const double* pb, int ldb,
                                       int K) {
   const int l = threadIdx.x & 63;
-  double av[12], bv[12];
+  const double* qa = pa + (l & 15) * lda + (l >> 4);
+  const double* qb = pb + (l >> 4) * ldb + (l & 15);
+#pragma unroll 1
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    double av[4], bv[4];
 #pragma unroll
-  for (int s = 0; s < 12; ++s) {
-    if (4 * s < K) {
-      av[s] = pa[(l & 15) * lda + 4 * s + (l >> 4)];
-      bv[s] = pb[(4 * s + (l >> 4)) * ldb + (l & 15)];
+    for (int s = 0; s < 4; ++s) {
+      av[s] = qa[k0 + 4 * s];
+      bv[s] = qb[(k0 + 4 * s) * ldb];
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[s], bv[s], acc, 0, 0, 0);
+  }
+}
+
+// The same with a compile-time depth: every operand load is issued first.
+template <int K>
+__device__ __forceinline__ void mma16k(d4& acc, const double* pa, int lda, const double* pb, int ldb) {
+  if constexpr (K > 0) {
+    const int l = threadIdx.x & 63;
+    const double* qa = pa + (l & 15) * lda + (l >> 4);
+    const double* qb = pb + (l >> 4) * ldb + (l & 15);
+    double av[K / 4], bv[K / 4];
+#pragma unroll
+    for (int s = 0; s < K / 4; ++s) {
+      av[s] = qa[4 * s];
+      bv[s] = qb[4 * s * ldb];
+    }
+#pragma unroll
+    for (int s = 0; s < K / 4; ++s) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[s], bv[s], acc, 0, 0, 0);
+  }
+}
+
+// Per-lane constants of a band sweep.
+struct Band {
+  int w, l, p, q, br, gi0, gj0;
+  double l10;      // L[br+1][br]
+  double dl[2];    // 1 / lamL of the lane's two rows
+};
+
+// Sub-tile (w, C) of the band: wait for the band above, add the in-tile
+// feedback of the finished sub-tiles above and to the left, run Algorithm 3
+// on the 16 x 16 block, publish E and C, write the outputs.
+template <typename T, int C>
+__device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, const Band& b,
+                                         double (&Dc)[2][2], double (&Rc)[2][2], const double (&dc)[2],
+                                         double& part, int& bad) {
+  const int w = b.w, l = b.l, p = b.p, q = b.q, br = b.br;
+  constexpr int uc = SS * C;
+  // the band above must have finished sub-tile C
+  if (w > 0) {
+    int spins = 0;
+    while (__hip_atomic_load(&sm.done[w - 1], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) <= C) {
+      __builtin_amdgcn_s_sleep(1);
+      if (++spins > (1 << 22)) {
+        bad |= FLAG_TIMEOUT;
+        break;
+      }
     }
   }
+  // feedback from the finished sub-tiles above (same column) and to the left
+  // (same band) inside this tile
+  {
+    d4 aD = {0.0, 0.0, 0.0, 0.0}, aR = {0.0, 0.0, 0.0, 0.0};
+    mma16k<SS * C>(aR, &sm.x.t.Ct[SS * w][0], TP, &sm.Us[0][uc], TP);
+    mma16(aD, &sm.Ls[SS * w][0], TP, &sm.x.t.Et[0][uc], TP, SS * w);
+    double(*sc)[SS + 1] = sm.scr[w];
 #pragma unroll
-  for (int s = 0; s < 12; ++s)
-    if (4 * s < K) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[s], bv[s], acc, 0, 0, 0);
+    for (int r = 0; r < 4; ++r) sc[4 * r + (l >> 4)][l & 15] = aD[r];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) Dc[i][j] += sc[2 * p + i][2 * q + j];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sc[4 * r + (l >> 4)][l & 15] = aR[r];
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) Rc[i][j] += sc[2 * p + i][2 * q + j];
+    __builtin_amdgcn_wave_barrier();
+  }
+
+  // Algorithm 3 on the 16 x 16 sub-tile, one 2 x 2 block per lane. The
+  // blocks form an 8 x 8 grid swept along its anti-diagonals: in step k the
+  // lanes with p + q == k round their four entries (an in-block chain of
+  // three entry anti-diagonals), and every lane first adds the feedback of
+  // the blocks finished in step k-1 in its block column (errors through L,
+  // Alg. 3 push down) and block row (C through U, push right). Finished
+  // blocks publish E and C into Et / Ct, read back in the next step by the
+  // same wave (LDS is in order within a wave: no barrier).
+  const double u01 = sm.Us[uc + 2 * q][uc + 2 * q + 1];
+  double yf[2][2], cf[2][2];
+#pragma unroll 1
+  for (int k = 0; k < SS - 1; ++k) {
+    const int sr = k - 1 - q, sc = k - 1 - p;  // source block row / column
+    const bool vr = sr >= 0 && sr < SS / 2, vc = sc >= 0 && sc < SS / 2;
+    const int er = SS * w + 2 * (vr ? sr : 0);  // tile row of the source errors
+    const int lc = vr ? er : TB;                 // L column (zero column if none)
+    const int cc = uc + 2 * (vc ? sc : 0);       // tile column of the source C
+    const int ur = vc ? cc : TB;                 // U row (zero row if none)
+    const double2 e0 = *reinterpret_cast<const double2*>(&sm.x.t.Et[er][uc + 2 * q]);
+    const double2 e1 = *reinterpret_cast<const double2*>(&sm.x.t.Et[er + 1][uc + 2 * q]);
+    const double2 l0 = *reinterpret_cast<const double2*>(&sm.Ls[br][lc]);
+    const double2 l1 = *reinterpret_cast<const double2*>(&sm.Ls[br + 1][lc]);
+    const double2 c0 = *reinterpret_cast<const double2*>(&sm.x.t.Ct[br][cc]);
+    const double2 c1 = *reinterpret_cast<const double2*>(&sm.x.t.Ct[br + 1][cc]);
+    const double2 v0 = *reinterpret_cast<const double2*>(&sm.Us[ur][uc + 2 * q]);
+    const double2 v1 = *reinterpret_cast<const double2*>(&sm.Us[ur + 1][uc + 2 * q]);
+    Dc[0][0] = fma(l0.y, e1.x, fma(l0.x, e0.x, Dc[0][0]));
+    Dc[0][1] = fma(l0.y, e1.y, fma(l0.x, e0.y, Dc[0][1]));
+    Dc[1][0] = fma(l1.y, e1.x, fma(l1.x, e0.x, Dc[1][0]));
+    Dc[1][1] = fma(l1.y, e1.y, fma(l1.x, e0.y, Dc[1][1]));
+    Rc[0][0] = fma(c0.y, v1.x, fma(c0.x, v0.x, Rc[0][0]));
+    Rc[0][1] = fma(c0.y, v1.y, fma(c0.x, v0.y, Rc[0][1]));
+    Rc[1][0] = fma(c1.y, v1.x, fma(c1.x, v0.x, Rc[1][0]));
+    Rc[1][1] = fma(c1.y, v1.y, fma(c1.x, v0.y, Rc[1][1]));
+    if (p + q == k) {
+      const double y00 = Rc[0][0] + Dc[0][0];
+      const double e00 = rint(y00) - y00;
+      const double c00 = Dc[0][0] + e00;
+      const double d10 = fma(b.l10, e00, Dc[1][0]);
+      const double y01 = fma(c00, u01, Rc[0][1]) + Dc[0][1];
+      const double e01 = rint(y01) - y01;
+      const double c01 = Dc[0][1] + e01;
+      const double y10 = Rc[1][0] + d10;
+      const double e10 = rint(y10) - y10;
+      const double c10 = d10 + e10;
+      const double d11 = fma(b.l10, e01, Dc[1][1]);
+      const double y11 = fma(c10, u01, Rc[1][1]) + d11;
+      const double e11 = rint(y11) - y11;
+      const double c11 = d11 + e11;
+      *reinterpret_cast<double2*>(&sm.x.t.Et[br][uc + 2 * q]) = double2{e00, e01};
+      *reinterpret_cast<double2*>(&sm.x.t.Et[br + 1][uc + 2 * q]) = double2{e10, e11};
+      *reinterpret_cast<double2*>(&sm.x.t.Ct[br][uc + 2 * q]) = double2{c00, c01};
+      *reinterpret_cast<double2*>(&sm.x.t.Ct[br + 1][uc + 2 * q]) = double2{c10, c11};
+      yf[0][0] = y00; yf[0][1] = y01; yf[1][0] = y10; yf[1][1] = y11;
+      cf[0][0] = c00; cf[0][1] = c01; cf[1][0] = c10; cf[1][1] = c11;
+    }
+  }
+
+  // hand-off to the band below, then the global outputs
+  __hip_atomic_store(&sm.done[w], C + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  T* Y = (T*)a.Y;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int gi = b.gi0 + br + i;
+    const int gj = b.gj0 + uc + 2 * q;
+    double ev[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) ev[j] = rint(yf[i][j]) - yf[i][j];
+    *reinterpret_cast<double2*>(a.E + (int64_t)gi * a.np + gj) = double2{ev[0], ev[1]};
+    *reinterpret_cast<double2*>(a.C + (int64_t)gi * a.np + gj) = double2{cf[i][0], cf[i][1]};
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const double yv = yf[i][j];
+      const double z = rint(yv);
+      if (gi < a.m && gj + j < a.n) {
+        if (!isfinite(yv)) bad |= FLAG_NONFINITE;
+        else if (fabs(z) > 2147483647.0) bad |= FLAG_OVERFLOW;
+        const double zc = fmin(fmax(z, -2147483648.0), 2147483647.0);
+        a.Z[(int64_t)gi * a.ldz + gj + j] = isfinite(zc) ? (int32_t)zc : 0;
+        if (Y) Y[(int64_t)gi * a.ldy + gj + j] = (T)yv;
+        part += ev[j] * ev[j] * b.dl[i] * dc[j];
+      }
+    }
+  }
 }
 
 // Sweep of one tile. Wave w owns the 16-row band 16w .. 16w+15 and sweeps its
@@ -164,11 +320,13 @@ __device__ __forceinline__ void mma16(d4& acc, const double* pa, int lda, const 
 // barrier). Sub-tile (w, c) starts when the band above has finished
 // sub-tile c; the feedback from the finished sub-tiles above and to the left
 // is added first as two small MFMA products. Lane l owns the 2 x 2 block at
-// band rows 2p, 2p+1 (p = l & 7) and sub-tile columns 2q, 2q+1 (q = l >> 3).
+// band rows 2p, 2p+1 (p = l >> 3) and sub-tile columns 2q, 2q+1 (q = l & 7):
+// eight consecutive lanes read eight different column pairs of a factor row,
+// which keeps the LDS window reads free of bank conflicts.
 template <typename T>
 __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
-  const int p = l & 7, q = l >> 3;
+  const int p = l >> 3, q = l & 7;
   const int br = SS * w + 2 * p;  // tile row of the lane's first row
   const int gi0 = I * TB, gj0 = J * TB;
   const T* X = (const T*)a.X;
@@ -188,18 +346,49 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   for (int c = 0; c < 4; ++c)
 #pragma unroll
     for (int j = 0; j < 2; ++j) du[c][j] = a.dU[gj0 + SS * c + 2 * q + j];
+  // X, then the accumulated right (R, from tile column 2 on) and down (P,
+  // from tile row 2 on) feedback; each group is issued as one batch
 #pragma unroll
   for (int c = 0; c < 4; ++c)
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int gi = gi0 + br + i, gj = gj0 + SS * c + 2 * q + j;
-        double r = load_x<T>(X, a.ldx, gi, gj, a.m, a.n);
-        if (J >= 2) r += a.R[(int64_t)gi * a.np + gj];
-        Rt[c][i][j] = r;
-        Dn[c][i][j] = (I >= 2) ? a.P[(int64_t)gi * a.np + gj] : 0.0;
-      }
+      for (int j = 0; j < 2; ++j)
+        Rt[c][i][j] = load_x<T>(X, a.ldx, gi0 + br + i, gj0 + SS * c + 2 * q + j, a.m, a.n);
+  double2 rv[4][2], pv[4][2];
+  if (J >= 2) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        rv[c][i] = *reinterpret_cast<const double2*>(a.R + (int64_t)(gi0 + br + i) * a.np + gj0 + SS * c + 2 * q);
+  } else {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) rv[c][i] = double2{0.0, 0.0};
+  }
+  if (I >= 2) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        pv[c][i] = *reinterpret_cast<const double2*>(a.P + (int64_t)(gi0 + br + i) * a.np + gj0 + SS * c + 2 * q);
+  } else {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) pv[c][i] = double2{0.0, 0.0};
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      Rt[c][i][0] += rv[c][i].x;
+      Rt[c][i][1] += rv[c][i].y;
+      Dn[c][i][0] = pv[c][i].x;
+      Dn[c][i][1] = pv[c][i].y;
+    }
 #pragma unroll
   for (int s = 0; s < 16; ++s) {
     const int e = t + NT * s, r = e >> 6, x = e & 63;
@@ -207,12 +396,9 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
     sm.Us[r][x] = uv[s];
   }
   if (t < TB) {
-    sm.Ls[t][TB] = 0.0;
+    *reinterpret_cast<double2*>(&sm.Ls[t][TB]) = double2{0.0, 0.0};
     sm.Us[TB][t] = 0.0;
-  }
-  if (t < 4 * SS) {
-    sm.xe[t >> 4][t & 15] = 0.0;
-    sm.xc[t >> 4][t & 15] = 0.0;
+    sm.Us[TB + 1][t] = 0.0;
   }
   if (t < 4) sm.done[t] = 0;
 
@@ -258,159 +444,26 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
         for (int j = 0; j < 2; ++j) Rt[c][i][j] += sm.x.T[br + i][SS * c + 2 * q + j];
   }
   __syncthreads();
+  // the band's rows of Et / Ct start at zero: the block sweep reads a
+  // (zero-weighted) source block before it is written
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    const int e = l + 64 * s, r = SS * w + (e >> 5), x = 2 * (e & 31);
+    *reinterpret_cast<double2*>(&sm.x.t.Et[r][x]) = double2{0.0, 0.0};
+    *reinterpret_cast<double2*>(&sm.x.t.Ct[r][x]) = double2{0.0, 0.0};
+  }
+  Band bd;
+  bd.w = w; bd.l = l; bd.p = p; bd.q = q; bd.br = br; bd.gi0 = gi0; bd.gj0 = gj0;
+  bd.l10 = sm.Ls[br + 1][br];
+  bd.dl[0] = dl[0];
+  bd.dl[1] = dl[1];
 
   double part = 0.0;
   int bad = 0;
-  T* Y = (T*)a.Y;
-  const int pq2 = 2 * (p + q);
-#pragma unroll 1
-  for (int c = 0; c < 4; ++c) {
-    // this sub-tile's share of the band state (kept rolled: small code)
-    double Dc[2][2], Rc[2][2], dc[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        Dc[i][j] = c == 0 ? Dn[0][i][j] : c == 1 ? Dn[1][i][j] : c == 2 ? Dn[2][i][j] : Dn[3][i][j];
-        Rc[i][j] = c == 0 ? Rt[0][i][j] : c == 1 ? Rt[1][i][j] : c == 2 ? Rt[2][i][j] : Rt[3][i][j];
-      }
-#pragma unroll
-    for (int j = 0; j < 2; ++j) dc[j] = c == 0 ? du[0][j] : c == 1 ? du[1][j] : c == 2 ? du[2][j] : du[3][j];
-    // the band above must have finished sub-tile c
-    if (w > 0) {
-      int spins = 0;
-      while (__hip_atomic_load(&sm.done[w - 1], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) <= c) {
-        __builtin_amdgcn_s_sleep(1);
-        if (++spins > (1 << 22)) {
-          bad |= FLAG_TIMEOUT;
-          break;
-        }
-      }
-    }
-    // feedback from the finished sub-tiles above (same column) and to the
-    // left (same band) inside this tile
-    {
-      d4 aD = {0.0, 0.0, 0.0, 0.0}, aR = {0.0, 0.0, 0.0, 0.0};
-      mma16(aD, &sm.Ls[SS * w][0], TP, &sm.x.t.Et[0][SS * c], TP, SS * w);
-      mma16(aR, &sm.x.t.Ct[SS * w][0], TP, &sm.Us[0][SS * c], TP, SS * c);
-      double(*sc)[SS + 1] = sm.scr[w];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sc[4 * r + (l >> 4)][l & 15] = aD[r];
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) Dc[i][j] += sc[2 * p + i][2 * q + j];
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sc[4 * r + (l >> 4)][l & 15] = aR[r];
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) Rc[i][j] += sc[2 * p + i][2 * q + j];
-      __builtin_amdgcn_wave_barrier();
-    }
-
-    // Algorithm 3 on the 16 x 16 sub-tile. Iteration d applies the pushes of
-    // anti-diagonal d-1 and rounds the entries on anti-diagonal d; the two
-    // pushes that complete an entry about to be rounded are applied first.
-    // Window slot (x & 1) of Lw holds L[br+i][16w+x], slot (y & 1) of Uw holds
-    // U[16c+y][16c+2q+j]; the entries of anti-diagonal d are loaded in
-    // iteration d and committed after its pushes.
-    const int lr = SS * w, uc = SS * c;
-    double Lw[2][2] = {{0.0, 0.0}, {0.0, 0.0}}, Uw[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
-    double yf[2][2] = {{0.0, 0.0}, {0.0, 0.0}}, cf[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
-    double* xe = sm.xe[w];
-    double* xc = sm.xc[w];
-#pragma unroll 1
-    for (int D2 = 0; D2 < SS; ++D2) {
-#pragma unroll
-      for (int dd = 0; dd < 2; ++dd) {
-        const int d = 2 * D2 + dd;
-        if (d <= 2 * SS - 2) {
-          const int ps = dd ^ 1;  // window slot of anti-diagonal d-1
-          const double e0 = xe[2 * q], e1 = xe[2 * q + 1];
-          const double c0 = xc[2 * p], c1 = xc[2 * p + 1];
-          const double e2[2] = {e0, e1}, c2[2] = {c0, c1};
-          const int x = d - 2 * q, y = d - 2 * p;
-          const int xi = (x >= 0 && x < SS) ? lr + x : TB;
-          const int yi = (y >= 0 && y < SS) ? uc + y : TB;
-          const double Ln[2] = {sm.Ls[br][xi], sm.Ls[br + 1][xi]};
-          const double Un[2] = {sm.Us[yi][uc + 2 * q], sm.Us[yi][uc + 2 * q + 1]};
-#define G2D_ROUND(I_, J_)                                                        \
-  {                                                                              \
-    const double dn = Dc[I_][J_] + Lw[(ps - (J_)) & 1][I_] * e2[J_];          \
-    const double rt = Rc[I_][J_] + c2[I_] * Uw[(ps - (I_)) & 1][J_];          \
-    const double yv = rt + dn;                                                   \
-    const double z = rint(yv);                                                   \
-    const double ev = z - yv;                                                    \
-    const double cv = dn + ev;                                                   \
-    yf[I_][J_] = yv;                                                             \
-    cf[I_][J_] = cv;                                                             \
-    xe[2 * q + (J_)] = ev;                                                       \
-    xc[2 * p + (I_)] = cv;                                                       \
-  }
-          if (dd == 0) {
-            if (d == pq2) G2D_ROUND(0, 0)
-            if (d == pq2 + 2) G2D_ROUND(1, 1)
-          } else {
-            if (d == pq2 + 1) {
-              G2D_ROUND(0, 1)
-              G2D_ROUND(1, 0)
-            }
-          }
-#undef G2D_ROUND
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-              Dc[i][j] += Lw[(ps - j) & 1][i] * e2[j];  // push down
-              Rc[i][j] += c2[i] * Uw[(ps - i) & 1][j];  // push right
-            }
-#pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            Lw[dd][i] = Ln[i];
-            Uw[dd][i] = Un[i];
-          }
-          __builtin_amdgcn_wave_barrier();
-        }
-      }
-    }
-
-    // results of sub-tile (w, c): E and C into LDS for the sub-tiles below
-    // and to the right, then the hand-off, then the global outputs
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const double yv = yf[i][j];
-        sm.x.t.Et[br + i][SS * c + 2 * q + j] = rint(yv) - yv;
-        sm.x.t.Ct[br + i][SS * c + 2 * q + j] = cf[i][j];
-      }
-    __hip_atomic_store(&sm.done[w], c + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int gi = gi0 + br + i;
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int gj = gj0 + SS * c + 2 * q + j;
-        const double yv = yf[i][j];
-        const double z = rint(yv);
-        const double e = z - yv;
-        a.E[(int64_t)gi * a.np + gj] = e;
-        a.C[(int64_t)gi * a.np + gj] = cf[i][j];
-        if (gi < a.m && gj < a.n) {
-          if (!isfinite(yv)) bad |= FLAG_NONFINITE;
-          else if (fabs(z) > 2147483647.0) bad |= FLAG_OVERFLOW;
-          const double zc = fmin(fmax(z, -2147483648.0), 2147483647.0);
-          a.Z[(int64_t)gi * a.ldz + gj] = isfinite(zc) ? (int32_t)zc : 0;
-          if (Y) Y[(int64_t)gi * a.ldy + gj] = (T)yv;
-          part += e * e * dl[i] * dc[j];
-        }
-      }
-    }
-  }
+  sub_tile<T, 0>(a, sm, bd, Dn[0], Rt[0], du[0], part, bad);
+  sub_tile<T, 1>(a, sm, bd, Dn[1], Rt[1], du[1], part, bad);
+  sub_tile<T, 2>(a, sm, bd, Dn[2], Rt[2], du[2], part, bad);
+  sub_tile<T, 3>(a, sm, bd, Dn[3], Rt[3], du[3], part, bad);
 
   if (bad) raise_flag(a.flags, bad);
 #pragma unroll
