@@ -160,89 +160,206 @@ __global__ __launch_bounds__(NT) void k_gram(FacArgs f, const T* A, int64_t lda,
 // ---------------------------------------------------------------------------
 // Cholesky of one 64 x 64 diagonal block (already updated by all earlier
 // panels) and the inverse of its lower factor; one workgroup per side.
-// Thread (c, g), c = t & 63, g = t >> 6, keeps rows g + 4u of column c in
-// registers. The pivot loops are unrolled so every register index is a
-// constant; each pivot column / row is broadcast through a buffer that
-// alternates between steps. A pivot that is not positive and finite raises
-// FLAG_SINGULAR and is replaced by 1 so the remaining work stays finite.
+//
+// Blocked over 16 x 16 sub-blocks held in LDS. For each diagonal sub-block k:
+// one wave factors it and inverts the factor in registers (16 pivots, each
+// broadcast by DPP); the other sub-blocks
+// of column k are solved against that inverse and the trailing sub-blocks
+// updated, both as 16 x 16 MFMA products. The inverse of the whole factor is
+// then assembled block row by block row:
+//   W_ij = -W_ii (sum_{k=j}^{i-1} L_ik W_kj).
+// A pivot that is not positive and finite raises FLAG_SINGULAR and is
+// replaced by 1 so the remaining work stays finite.
 // ---------------------------------------------------------------------------
+
+constexpr int DS = 16;  // sub-block edge
+
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+  const long long x = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane((int)x, lane);
+  const int hi = __builtin_amdgcn_readlane((int)(x >> 32), lane);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// 1 / sqrt(x) for x > 0: hardware estimate and one Newton step.
+__device__ __forceinline__ double rsqrt_nr(double x) {
+  const double y = __builtin_amdgcn_rsq(x);
+  const double h = 0.5 * x;
+  return y * fma(-h * y, y, 1.5);
+}
+
+// acc += s * X (16 x K) op(Y) on MFMA; X and Y in LDS, row-major with strides
+// ldx, ldy; op(Y) = Y^T with Y given as 16 x K (T = 1) or Y itself, K x 16
+// (T = 0). One wave; every operand load is issued before the first MFMA.
+template <int K, int T>
+__device__ __forceinline__ void mfma_lds(d4& acc, const double* X, int ldx, const double* Y, int ldy,
+                                         double sgn) {
+  const int l = threadIdx.x & 63;
+  const double* qx = X + (l & 15) * ldx + (l >> 4);
+  double xv[K / 4], yv[K / 4];
+#pragma unroll
+  for (int s = 0; s < K / 4; ++s) {
+    xv[s] = sgn * qx[4 * s];
+    yv[s] = T ? Y[(l & 15) * ldy + (l >> 4) + 4 * s] : Y[((l >> 4) + 4 * s) * ldy + (l & 15)];
+  }
+#pragma unroll
+  for (int s = 0; s < K / 4; ++s) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xv[s], yv[s], acc, 0, 0, 0);
+}
+
+// MFMA-layout accumulator <-> a 16 x 16 LDS block (element r of lane l is
+// entry (4r + l/16, l%16)).
+__device__ __forceinline__ void d4_load(d4& acc, const double* P, int ld) {
+  const int l = threadIdx.x & 63;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) acc[r] = P[(4 * r + (l >> 4)) * ld + (l & 15)];
+}
+__device__ __forceinline__ void d4_store(const d4& acc, double* P, int ld) {
+  const int l = threadIdx.x & 63;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) P[(4 * r + (l >> 4)) * ld + (l & 15)] = acc[r];
+}
+
+// v of lane `lane` (0..15, a constant after unrolling) of every 16-lane row,
+// broadcast to the whole row (DPP row_newbcast), for a double.
+__device__ __forceinline__ double bcast16(double v, int lane) {
+  const long long x = __double_as_longlong(v);
+  int lo = (int)x, hi = (int)(x >> 32);
+#define G2D_BC(L_)                                                  \
+  case L_:                                                          \
+    lo = __builtin_amdgcn_mov_dpp(lo, 0x150 + (L_), 0xf, 0xf, false); \
+    hi = __builtin_amdgcn_mov_dpp(hi, 0x150 + (L_), 0xf, 0xf, false); \
+    break;
+  switch (lane) {
+    G2D_BC(0) G2D_BC(1) G2D_BC(2) G2D_BC(3) G2D_BC(4) G2D_BC(5) G2D_BC(6) G2D_BC(7)
+    G2D_BC(8) G2D_BC(9) G2D_BC(10) G2D_BC(11) G2D_BC(12) G2D_BC(13) G2D_BC(14) G2D_BC(15)
+    default: break;
+  }
+#undef G2D_BC
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Factor the 16 x 16 diagonal sub-block at A (stride lda, lower part valid)
+// in place and write its inverse to W (stride ldw). One wave; lane x of
+// every 16-lane row holds column x of the symmetric block and column x of
+// the inverse in registers, and every broadcast is a DPP broadcast of one
+// lane within the row. Pivot j:
+//   - the column j of L is broadcast: L[r][j] = S[r][j] / sqrt(S[j][j]),
+//     and written out (zeros above the diagonal) by lane j;
+//   - lane x's entry j becomes L[x][j] (by symmetry), and every lane
+//     subtracts L[r][j] L[x][j] from its entries r > j (right-looking
+//     Cholesky; lanes x <= j only touch columns already written out);
+//   - every lane advances the column-oriented forward substitution of
+//     L W = I with the same column: w[j] /= L[j][j], w[r] -= L[r][j] w[j].
+__device__ void chol_inv16(double* A, int lda, double* W, int ldw, int* flags) {
+  int l = threadIdx.x & 63;
+  // opaque to the optimiser: keeps the per-lane set-up inside the caller's
+  // loop instead of hoisting it out and holding it in registers throughout
+  asm volatile("" : "+v"(l));
+  const int x = l & 15;
+  double a[DS], w[DS];
+#pragma unroll
+  for (int r = 0; r < DS; ++r) {
+    a[r] = (r >= x) ? A[r * lda + x] : A[x * lda + r];
+    w[r] = (r == x) ? 1.0 : 0.0;
+  }
+  __builtin_amdgcn_wave_barrier();
+  bool bad = false;
+#pragma unroll
+  for (int j = 0; j < DS; ++j) {
+    double piv = bcast16(a[j], j);
+    const bool ok = piv > 0.0 && isfinite(piv);
+    bad |= !ok;
+    piv = ok ? piv : 1.0;
+    const double rs = rsqrt_nr(piv);
+    a[j] *= rs;
+    w[j] *= rs;
+    const double na = -a[j], nw = -w[j];
+    double lc[DS];
+#pragma unroll
+    for (int r = j + 1; r < DS; ++r) lc[r] = bcast16(a[r], j) * rs;
+    if (l == j) {
+#pragma unroll
+      for (int r = 0; r < DS; ++r) A[r * lda + j] = r < j ? 0.0 : (r == j ? a[j] : lc[r]);
+    }
+#pragma unroll
+    for (int r = j + 1; r < DS; ++r) {
+      a[r] = fma(lc[r], na, a[r]);
+      w[r] = fma(lc[r], nw, w[r]);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep each pivot's broadcasts local (register pressure)
+  }
+  if (bad && l == 0) raise_flag(flags, FLAG_SINGULAR);
+  if (l < DS) {
+#pragma unroll
+    for (int r = 0; r < DS; ++r) W[r * ldw + x] = (r >= x) ? w[r] : 0.0;
+  }
+}
 
 __global__ __launch_bounds__(NT) void k_diag(FacArgs f, int kb) {
   const Side& sd = f.s[blockIdx.x];
   if (kb >= sd.nb) return;
-  __shared__ double S[TB][TB + 1];
-  __shared__ double col[2][TB];
-  __shared__ double rd[TB];
-  const int t = threadIdx.x, c = t & 63, g = t >> 6;
+  constexpr int LD = TB + 1;
+  __shared__ double Am[TB][LD];      // the block, becomes Lc (lower)
+  __shared__ double Wm[TB][LD];      // Lc^{-1} (lower)
+  __shared__ double Tm[4][DS][DS + 1];
+  const int t = threadIdx.x, w = t >> 6;
   double* blk = sd.gr + (int64_t)kb * TB * sd.dp + (int64_t)kb * TB;
-  // a[u] is entry (g + 4u, c); the upper triangle starts at zero. Updates are
-  // applied to every row of a thread without masking: entries above the
-  // diagonal collect finite junk that no valid entry ever reads, and they are
-  // written out as zero.
-  double a[16];
+  {
+    double x[16];
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const double x = blk[(int64_t)(g + 4 * u) * sd.dp + c];
-    a[u] = (g + 4 * u >= c) ? x : 0.0;
-  }
-#pragma unroll 1
-  for (int j = 0; j < TB; ++j) {
-    double* cj = col[j & 1];
-    if (c == j) {  // publish column j before its scaling; cj[j] is the pivot
-#pragma unroll
-      for (int u = 0; u < 16; ++u) cj[g + 4 * u] = a[u];
+    for (int s = 0; s < 16; ++s) {
+      const int e = t + NT * s;
+      x[s] = blk[(int64_t)(e >> 6) * sd.dp + (e & 63)];
     }
-    __syncthreads();
-    double piv = cj[j];
-    if (!(piv > 0.0) || !isfinite(piv)) {
-      if (t == 0) raise_flag(f.flags, FLAG_SINGULAR);
-      piv = 1.0;
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+      const int e = t + NT * s, r = e >> 6, c = e & 63;
+      Am[r][c] = (c <= r) ? x[s] : 0.0;
+      Wm[r][c] = 0.0;
     }
-    if (c == j) {  // L[i][j] = a_ij / sqrt(piv)
-      const double rsq = 1.0 / sqrt(piv);
-#pragma unroll
-      for (int u = 0; u < 16; ++u) a[u] *= rsq;
-    } else if (c > j) {  // a_ic -= L[i][j] L[c][j] = a_ij a_cj / piv
-      const double cc = cj[c] / piv;
-#pragma unroll
-      for (int u = 0; u < 16; ++u) a[u] = fma(-cj[g + 4 * u], cc, a[u]);
-    }
-  }
-  // Lc into LDS: strictly lower part in S, reciprocal of the diagonal in rd
-#pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int i = g + 4 * u;
-    S[i][c] = (c < i) ? a[u] : 0.0;
-    if (c == i) rd[i] = 1.0 / a[u];
-    blk[(int64_t)i * sd.dp + c] = (c <= i) ? a[u] : 0.0;
   }
   __syncthreads();
-  // V = Lc^{-1} by forward substitution on the identity, one pivot row per
-  // step; v[u] holds row g + 4(u + U) of column c (window shifting with U);
-  // rows past the block hold finite junk and are never stored.
-  double* dv = sd.dinv + (int64_t)kb * TB * TB;
-  double v[16];
-#pragma unroll
-  for (int u = 0; u < 16; ++u) v[u] = (g + 4 * u == c) ? 1.0 : 0.0;
-#pragma unroll 1
-  for (int U = 0; U < 16; ++U) {
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int k = 4 * U + kk;
-      double* rk = col[kk & 1];
-      if (g == kk) {
-        v[0] *= rd[k];
-        rk[c] = v[0];
-      }
-      __syncthreads();
-      const double x = rk[c];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = fma(-S[(g + 4 * (u + U)) & 63][k], x, v[u]);
+  for (int k = 0; k < 4; ++k) {
+    const int o = DS * k;
+    if (w == k) chol_inv16(&Am[o][o], LD, &Wm[o][o], LD, f.flags);
+    __syncthreads();
+    if (w > k) {  // panel: L_wk = A_wk W_kk^T
+      d4 acc = {0.0, 0.0, 0.0, 0.0};
+      mfma_lds<DS, 1>(acc, &Am[DS * w][o], LD, &Wm[o][o], LD, 1.0);
+      __builtin_amdgcn_wave_barrier();
+      d4_store(acc, &Am[DS * w][o], LD);
     }
-    const int i = g + 4 * U;
-    dv[i * TB + c] = (c <= i) ? v[0] : 0.0;
+    __syncthreads();
+    if (w > k) {  // trailing: A_wj -= L_wk L_jk^T, k < j <= w
+      for (int j = k + 1; j <= w; ++j) {
+        d4 acc;
+        d4_load(acc, &Am[DS * w][DS * j], LD);
+        mfma_lds<DS, 1>(acc, &Am[DS * w][o], LD, &Am[DS * j][o], LD, -1.0);
+        d4_store(acc, &Am[DS * w][DS * j], LD);
+      }
+    }
+    __syncthreads();
+  }
+  // off-diagonal blocks of the inverse, block row by block row
+  for (int i = 1; i < 4; ++i) {
+    if (w < i) {
+      d4 acc = {0.0, 0.0, 0.0, 0.0};
+      for (int k = w; k < i; ++k)
+        mfma_lds<DS, 0>(acc, &Am[DS * i][DS * k], LD, &Wm[DS * k][DS * w], LD, 1.0);
+      d4_store(acc, &Tm[w][0][0], DS + 1);
+      __builtin_amdgcn_wave_barrier();
+      d4 acc2 = {0.0, 0.0, 0.0, 0.0};
+      mfma_lds<DS, 0>(acc2, &Wm[DS * i][DS * i], LD, &Tm[w][0][0], DS + 1, -1.0);
+      d4_store(acc2, &Wm[DS * i][DS * w], LD);
+    }
+    __syncthreads();
+  }
+  double* dv = sd.dinv + (int64_t)kb * TB * TB;
 #pragma unroll
-    for (int u = 0; u < 15; ++u) v[u] = v[u + 1];
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s, r = e >> 6, c = e & 63;
+    blk[(int64_t)r * sd.dp + c] = Am[r][c];
+    dv[e] = Wm[r][c];
   }
 }
 
