@@ -33,8 +33,7 @@ static int round_up(int v, int a) { return (v + a - 1) / a * a; }
 static void free_all(Factors* f) {
   for (void* p : f->allocations) (void)hipFree(p);
   f->allocations.clear();
-  if (f->sched.d_tasks) (void)hipFree(f->sched.d_tasks);
-  f->sched.d_tasks = nullptr;
+  free_schedule(f->sched);
 }
 
 static gptq2d_status alloc(Factors* f, void** p, size_t bytes) {
@@ -108,7 +107,8 @@ gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
       if (he != hipSuccess) st = hip_fail(he, "hipMemset");
     }
   }
-  if (st == GPTQ2D_OK) st = build_schedule(*f, env_int("GPTQ2D_BATCH", 4));
+  if (st == GPTQ2D_OK)
+    st = build_schedule(*f, env_int("GPTQ2D_BATCH", 4), env_int("GPTQ2D_PERSIST", 0) != 0);
   if (st != GPTQ2D_OK) {
     free_all(f);
     delete f;

@@ -51,7 +51,52 @@ struct StageArgs {
   int* flags;
   const int4* tasks;
   int stage, ilo, nsweep;
+  // persistent schedule: the work list, its cursor, per-tile completion
+  // flags, per-(tile, direction) delivery counters and their final values
+  const int4* items;
+  int nitems;
+  int* next;
+  int* tdone;
+  int* dcnt;
+  const int* expect;
 };
+
+// ---------------------------------------------------------------------------
+// Cross-workgroup hand-off of the persistent schedule. A producer makes its
+// global writes visible at device scope, then sets a counter; a consumer
+// polls the counter (bounded: a wait that never ends raises FLAG_TIMEOUT and
+// gives up, so every workgroup always finishes), then acquires.
+// ---------------------------------------------------------------------------
+constexpr int SPIN_LIMIT = 1 << 22;
+
+// Once any wait has timed out (FLAG_TIMEOUT in *flags) every other wait
+// gives up at once, so a broken hand-off costs one time-out, not one per item.
+__device__ __forceinline__ bool poll_geq(const int* p, int v, const int* flags) {
+  int spins = 0;
+  while (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < v) {
+    __builtin_amdgcn_s_sleep(2);
+    if (++spins > SPIN_LIMIT) return false;
+    if ((spins & 255) == 0 &&
+        (__hip_atomic_load(flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & FLAG_TIMEOUT))
+      return false;
+  }
+  return true;
+}
+
+// every thread of the workgroup; thread 0 sets *p = v after all threads'
+// earlier global writes are visible device-wide
+__device__ __forceinline__ void publish(int* p, int v) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// thread 0 has finished polling: make the producers' writes visible to the
+// whole workgroup
+__device__ __forceinline__ void acquire_all() {
+  if (threadIdx.x == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  __syncthreads();
+}
 
 constexpr int SS = 16;       // sub-tile edge of the in-tile sweep
 constexpr int TP = TB + 2;   // LDS row stride of the tile arrays (doubles)
@@ -97,8 +142,14 @@ __device__ __forceinline__ double load_x(const T* X, int64_t ldx, int gi, int gj
 
 // One deferred-feedback delivery (a GEMM task), 64-deep blocks double-buffered
 // through LDS: the loads of block b+1 are in flight while block b is on MFMA.
+// Task word: x = dir | overwrite << 1 | seq << 3 (seq: its place among the
+// deliveries into the same tile and direction), y = target tile row, z =
+// target tile column, w = first source | (one past last source) << 16. In
+// the persistent schedule (P) the task first waits for its source tiles and,
+// before touching the accumulator, for the deliveries ahead of it.
+template <bool P>
 __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
-  const int dir = tk.x & 1, ow = (tk.x >> 1) & 1;
+  const int dir = tk.x & 1, ow = (tk.x >> 1) & 1, seq = tk.x >> 3;
   const int ti = tk.y, tj = tk.z, s0 = tk.w & 0xffff, s1 = tk.w >> 16;
   const double* Ap;
   const double* Bp;
@@ -115,10 +166,20 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
     Bp = a.U + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
     out = a.R + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
   }
+  int* cnt = a.dcnt + 2 * (ti * a.NT + tj) + dir;
+  if (P) {
+    if (threadIdx.x == 0) {
+      bool ok = true;
+      for (int s = s0; s < s1 && ok; ++s)
+        ok = poll_geq(a.tdone + (dir == 0 ? s * a.NT + tj : ti * a.NT + s), 1, a.flags);
+      if (!ok) raise_flag(a.flags, FLAG_TIMEOUT);
+    }
+    acquire_all();
+  }
   const int64_t ldb = a.np;
   Acc acc;
   acc.zero();
-  if (!ow) acc_add_from(acc, out, a.np);
+  if (!P && !ow) acc_add_from(acc, out, a.np);
   double ra[16], rb[16];
   load_blk(Ap, lda, ra);
   load_blk(Bp, ldb, rb);
@@ -134,7 +195,14 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
     }
     mma_blk(acc, st);
   }
+  if (P) {
+    if (threadIdx.x == 0 && !poll_geq(cnt, seq, a.flags)) raise_flag(a.flags, FLAG_TIMEOUT);
+    acquire_all();
+    if (!ow) acc_add_from(acc, out, a.np);
+  }
   acc_store(acc, out, a.np, 1.0);
+  if (P) publish(cnt, seq + 1);
+  else __syncthreads();
 }
 
 // acc += A (16 x K) B (K x 16) on MFMA, both operands row-major in LDS with
@@ -323,13 +391,25 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
 // band rows 2p, 2p+1 (p = l >> 3) and sub-tile columns 2q, 2q+1 (q = l & 7):
 // eight consecutive lanes read eight different column pairs of a factor row,
 // which keeps the LDS window reads free of bank conflicts.
-template <typename T>
+template <typename T, bool P>
 __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   const int p = l >> 3, q = l & 7;
   const int br = SS * w + 2 * p;  // tile row of the lane's first row
   const int gi0 = I * TB, gj0 = J * TB;
   const T* X = (const T*)a.X;
+  if (P) {  // neighbours swept and every deferred delivery into this tile done
+    if (t == 0) {
+      const int tile = I * a.NT + J;
+      bool ok = true;
+      if (I >= 1) ok = ok && poll_geq(a.tdone + tile - a.NT, 1, a.flags);
+      if (J >= 1) ok = ok && poll_geq(a.tdone + tile - 1, 1, a.flags);
+      ok = ok && poll_geq(a.dcnt + 2 * tile, a.expect[2 * tile], a.flags);
+      ok = ok && poll_geq(a.dcnt + 2 * tile + 1, a.expect[2 * tile + 1], a.flags);
+      if (!ok) raise_flag(a.flags, FLAG_TIMEOUT);
+    }
+    acquire_all();
+  }
 
   // every global load of the prologue is issued before any is used
   double lv[16], uv[16], ga[16], gb[16];
@@ -471,6 +551,7 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   if (l == 0) sm.red[w] = part;
   __syncthreads();
   if (t == 0) a.objp[I * a.NT + J] = (sm.red[0] + sm.red[1]) + (sm.red[2] + sm.red[3]);
+  if (P) publish(a.tdone + I * a.NT + J, 1);
 }
 
 template <typename T>
@@ -479,10 +560,43 @@ __global__ __launch_bounds__(NT) void k_stage(StageArgs a) {
   const int b = blockIdx.x;
   if (b < a.nsweep) {
     const int I = a.ilo + b;
-    run_sweep<T>(a, I, a.stage - I, sm.s);
+    run_sweep<T, false>(a, I, a.stage - I, sm.s);
   } else {
-    run_task(a, a.tasks[b - a.nsweep], sm.t);
+    run_task<false>(a, a.tasks[b - a.nsweep], sm.t);
   }
+}
+
+// The whole sweep as one persistent launch: every workgroup takes the next
+// item of the work list (tile sweeps and deliveries in the order of the tile
+// anti-diagonals) until the list is exhausted. An item only waits for items
+// ahead of it in the list, and items are taken in list order, so the
+// earliest unfinished item always belongs to a running workgroup and can
+// proceed.
+template <typename T>
+__global__ __launch_bounds__(NT) void k_persist(StageArgs a) {
+  __shared__ StageSmem sm;
+  __shared__ int cur;
+  for (;;) {
+    if (threadIdx.x == 0) cur = atomicAdd(a.next, 1);
+    __syncthreads();
+    // the cursor must be a scalar: with a per-lane value the loop exit is
+    // divergent, and the compiler may then split the workgroup's lanes
+    // across iterations of a loop that contains barriers
+    const int idx = __builtin_amdgcn_readfirstlane(cur);
+    __syncthreads();
+    if (idx >= a.nitems) break;
+    const int4 it = a.items[idx];
+    if (it.x & 4) run_sweep<T, true>(a, it.y, it.z, sm.s);
+    else run_task<true>(a, it, sm.t);
+    // keeps the item's closing thread-0 store and the next cursor update in
+    // separate barrier intervals, so the two single-lane regions are never
+    // merged across the loop's back edge
+    __syncthreads();
+  }
+}
+
+__global__ void k_zero_ints(int* p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
 __global__ __launch_bounds__(NT) void k_obj_reduce(const double* part, int count, double* out) {
@@ -506,10 +620,14 @@ __global__ void k_zero_flags(int* p) {
 // Host side
 // ---------------------------------------------------------------------------
 
+static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+static int sync_ints(const Factors& f) { return 64 + 3 * f.MT * f.NT; }
+
 size_t workspace_bytes(const Factors& f) {
   const size_t tile = (size_t)f.mp * f.np * sizeof(double);
-  size_t objp = ((size_t)f.MT * f.NT * sizeof(double) + 255) / 256 * 256;
-  return 256 + objp + 4 * tile;
+  return 256 + align256((size_t)f.MT * f.NT * sizeof(double)) + 4 * tile +
+         align256((size_t)sync_ints(f) * sizeof(int));
 }
 
 Workspace workspace_carve(const Factors& f, void* base) {
@@ -518,12 +636,14 @@ Workspace workspace_carve(const Factors& f, void* base) {
   w.flags = (int*)p;
   p += 256;
   w.objp = (double*)p;
-  p += ((size_t)f.MT * f.NT * sizeof(double) + 255) / 256 * 256;
+  p += align256((size_t)f.MT * f.NT * sizeof(double));
   const size_t tile = (size_t)f.mp * f.np * sizeof(double);
   w.P = (double*)p;
   w.R = (double*)(p + tile);
   w.E = (double*)(p + 2 * tile);
   w.C = (double*)(p + 3 * tile);
+  w.sync = (int*)(p + 4 * tile);
+  w.nsync = sync_ints(f);
   return w;
 }
 
@@ -570,25 +690,59 @@ void schedule_tasks(int MT, int NTt, int g, std::vector<int4>& all, std::vector<
   off[S] = (int)all.size();
 }
 
-gptq2d_status build_schedule(Factors& f, int g) {
+void free_schedule(Schedule& sc) {
+  if (sc.d_tasks) (void)hipFree(sc.d_tasks);
+  if (sc.d_items) (void)hipFree(sc.d_items);
+  if (sc.d_expect) (void)hipFree(sc.d_expect);
+  sc.d_tasks = nullptr;
+  sc.d_items = nullptr;
+  sc.d_expect = nullptr;
+}
+
+template <typename V>
+static gptq2d_status upload(V** dst, const std::vector<V>& v, const char* what) {
+  if (v.empty()) return GPTQ2D_OK;
+  hipError_t e = hipMalloc(dst, v.size() * sizeof(V));
+  if (e != hipSuccess) return hip_fail(e, what);
+  e = hipMemcpy(*dst, v.data(), v.size() * sizeof(V), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, what);
+  return GPTQ2D_OK;
+}
+
+gptq2d_status build_schedule(Factors& f, int g, bool persist) {
   std::vector<int4> all;
   std::vector<int> off;
   if (g < 1) g = 1;
   schedule_tasks(f.MT, f.NT, g, all, off);
-  if (f.sched.d_tasks) {
-    (void)hipFree(f.sched.d_tasks);
-    f.sched.d_tasks = nullptr;
+  free_schedule(f.sched);
+  const int S = f.MT + f.NT - 1;
+  // the work list of the persistent form: per tile anti-diagonal k, its
+  // sweeps, then the tasks of launch k; seq numbers the deliveries into
+  // each (tile, direction) in list order
+  std::vector<int4> items;
+  std::vector<int> expect((size_t)2 * f.MT * f.NT, 0);
+  for (int k = 0; k < S; ++k) {
+    const int ilo = std::max(0, k - (f.NT - 1)), ihi = std::min(k, f.MT - 1);
+    for (int I = ilo; I <= ihi; ++I) items.push_back(make_int4(4, I, k - I, 0));
+    for (int i = off[k]; i < off[k + 1]; ++i) {
+      int4 tk = all[i];
+      int& cnt = expect[2 * (tk.y * f.NT + tk.z) + (tk.x & 1)];
+      tk.x = (tk.x & 3) | (cnt << 3);
+      all[i].x = tk.x;
+      ++cnt;
+      items.push_back(tk);
+    }
   }
-  if (!all.empty()) {
-    hipError_t e = hipMalloc(&f.sched.d_tasks, all.size() * sizeof(int4));
-    if (e != hipSuccess) return hip_fail(e, "schedule allocation");
-    e = hipMemcpy(f.sched.d_tasks, all.data(), all.size() * sizeof(int4), hipMemcpyHostToDevice);
-    if (e != hipSuccess) return hip_fail(e, "schedule upload");
-  }
+  gptq2d_status st = upload(&f.sched.d_tasks, all, "schedule upload");
+  if (st == GPTQ2D_OK && persist) st = upload(&f.sched.d_items, items, "work list upload");
+  if (st == GPTQ2D_OK && persist) st = upload(&f.sched.d_expect, expect, "work list upload");
+  if (st != GPTQ2D_OK) return st;
   f.sched.g = g;
-  f.sched.stages = f.MT + f.NT - 1;
+  f.sched.stages = S;
   f.sched.offset = off;
   f.sched.ntasks = all.size();
+  f.sched.persist = persist;
+  f.sched.nitems = (int)items.size();
   return GPTQ2D_OK;
 }
 
@@ -621,7 +775,22 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
   a.flags = ws.flags;
   hipLaunchKernelGGL(k_zero_flags, dim3(1), dim3(64), 0, s, ws.flags);
   const Schedule& S = f.sched;
-  for (int k = 0; k < S.stages; ++k) {
+  if (S.persist) {
+    a.items = S.d_items;
+    a.nitems = S.nitems;
+    a.next = ws.sync;
+    a.tdone = ws.sync + 64;
+    a.dcnt = ws.sync + 64 + f.MT * f.NT;
+    a.expect = S.d_expect;
+    hipLaunchKernelGGL(k_zero_ints, dim3(64), dim3(256), 0, s, ws.sync, ws.nsync);
+    int per_cu = 0, cus = 0, dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_persist<T>, NT, 0);
+    if (e != hipSuccess) return hip_fail(e, "occupancy query");
+    const int grid = std::max(1, std::min(S.nitems, std::max(per_cu, 1) * cus));
+    hipLaunchKernelGGL(k_persist<T>, dim3(grid), dim3(NT), 0, s, a);
+  } else for (int k = 0; k < S.stages; ++k) {
     const int ilo = std::max(0, k - (f.NT - 1)), ihi = std::min(k, f.MT - 1);
     a.stage = k;
     a.ilo = ilo;
