@@ -154,14 +154,16 @@ int gptq2d_version(void);
  * lazy block update of Sec. 4.3 on 64 x 64 tiles), for inspection and tests;
  * touches no device. Tiles: MT = ceil(m/64) rows, NT = ceil(n/64) columns;
  * launch k (0 <= k < MT+NT-1) sweeps the tiles with I + J = k. Each task is
- * four int32 {dir | overwrite << 1, target tile row, target tile column,
- * first source | (one past the last source) << 16}; dir 0 adds
- * L[I'][s] E[s][J] over source tile rows s to the down buffer of (I', J),
- * dir 1 adds C[I][s] U[s][J'] over source tile columns s to the right buffer
- * of (I, J'). offsets (host, MT+NT entries, nullable) receives the first task
+ * four int32 {dir | overwrite << 1 | (rows-1) << 2 | (cols-1) << 3,
+ * first target tile row, first target tile column,
+ * first source | (one past the last source) << 16}: it adds, to the block of
+ * rows x cols target tiles (1 or 2 each), the product over source tiles s of
+ * L[I][s] E[s][J] (dir 0, down buffer) or C[I][s] U[s][J] (dir 1, right
+ * buffer). offsets (host, MT+NT entries, nullable) receives the first task
  * of every launch and the total; tasks (host, 4*cap int32, nullable) the
- * first cap tasks in launch order. g is the batch width in tile
- * anti-diagonals (g >= 1). Returns the task count, or -1 on a bad argument. */
+ * first cap tasks in launch order. g is the batch width in source tiles of
+ * the far deliveries (g >= 1). Returns the task count, or -1 on a bad
+ * argument. */
 int64_t gptq2d_schedule_tasks(int m, int n, int g, int32_t* tasks, int64_t cap,
                               int32_t* offsets);
 

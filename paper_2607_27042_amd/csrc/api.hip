@@ -108,7 +108,7 @@ gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
     }
   }
   if (st == GPTQ2D_OK)
-    st = build_schedule(*f, env_int("GPTQ2D_BATCH", 4), env_int("GPTQ2D_PERSIST", 0) != 0);
+    st = build_schedule(*f, env_int("GPTQ2D_BATCH", 4));
   if (st != GPTQ2D_OK) {
     free_all(f);
     delete f;

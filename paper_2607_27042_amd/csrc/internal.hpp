@@ -12,20 +12,16 @@
 namespace g2d {
 
 // Deferred-feedback delivery of the blocked sweep: one GEMM task that adds the
-// contribution of a contiguous run of finished source tiles to one target
-// tile. x = dir | overwrite << 1, y = target tile row, z = target tile
-// column, w = first source | (one past last source) << 16.
+// contribution of a contiguous run of finished source tiles to a block of up
+// to 2 x 2 target tiles. x = dir | overwrite << 1 | (rows - 1) << 2 |
+// (cols - 1) << 3, y = first target tile row, z = first target tile column,
+// w = first source | (one past last source) << 16.
 struct Schedule {
   int g = 0;                     // batch width in tile anti-diagonals
   int stages = 0;                // tile anti-diagonals: MT + NT - 1
   std::vector<int> offset;       // per stage: first task (size stages + 1)
   int4* d_tasks = nullptr;       // all tasks, grouped by stage
   size_t ntasks = 0;
-  // persistent form: the same sweeps and tasks as one ordered work list
-  bool persist = false;
-  int4* d_items = nullptr;
-  int nitems = 0;
-  int* d_expect = nullptr;       // deliveries per (tile, direction)
 };
 
 struct Factors {
@@ -55,8 +51,6 @@ struct Workspace {
   double* R;     // deferred right feedback (columns to the left), mp x np
   double* E;     // rounding errors, mp x np
   double* C;     // the buffer C = L E, mp x np
-  int* sync;     // persistent schedule: cursor, tile flags, delivery counters
-  int nsync;     // ints in sync
 };
 size_t workspace_bytes(const Factors& f);
 Workspace workspace_carve(const Factors& f, void* base);
@@ -75,7 +69,7 @@ gptq2d_status launch_import(Factors& f, const double* L, int64_t ldl, const doub
 
 // sweep
 void schedule_tasks(int MT, int NT, int g, std::vector<int4>& all, std::vector<int>& offset);
-gptq2d_status build_schedule(Factors& f, int g, bool persist);
+gptq2d_status build_schedule(Factors& f, int g);
 void free_schedule(Schedule& s);
 gptq2d_status launch_round(const Factors& f, gptq2d_dtype dt, const void* X, int64_t ldx,
                            int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,

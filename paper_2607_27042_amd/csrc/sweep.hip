@@ -51,52 +51,7 @@ struct StageArgs {
   int* flags;
   const int4* tasks;
   int stage, ilo, nsweep;
-  // persistent schedule: the work list, its cursor, per-tile completion
-  // flags, per-(tile, direction) delivery counters and their final values
-  const int4* items;
-  int nitems;
-  int* next;
-  int* tdone;
-  int* dcnt;
-  const int* expect;
 };
-
-// ---------------------------------------------------------------------------
-// Cross-workgroup hand-off of the persistent schedule. A producer makes its
-// global writes visible at device scope, then sets a counter; a consumer
-// polls the counter (bounded: a wait that never ends raises FLAG_TIMEOUT and
-// gives up, so every workgroup always finishes), then acquires.
-// ---------------------------------------------------------------------------
-constexpr int SPIN_LIMIT = 1 << 22;
-
-// Once any wait has timed out (FLAG_TIMEOUT in *flags) every other wait
-// gives up at once, so a broken hand-off costs one time-out, not one per item.
-__device__ __forceinline__ bool poll_geq(const int* p, int v, const int* flags) {
-  int spins = 0;
-  while (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < v) {
-    __builtin_amdgcn_s_sleep(2);
-    if (++spins > SPIN_LIMIT) return false;
-    if ((spins & 255) == 0 &&
-        (__hip_atomic_load(flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & FLAG_TIMEOUT))
-      return false;
-  }
-  return true;
-}
-
-// every thread of the workgroup; thread 0 sets *p = v after all threads'
-// earlier global writes are visible device-wide
-__device__ __forceinline__ void publish(int* p, int v) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// thread 0 has finished polling: make the producers' writes visible to the
-// whole workgroup
-__device__ __forceinline__ void acquire_all() {
-  if (threadIdx.x == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  __syncthreads();
-}
 
 constexpr int SS = 16;       // sub-tile edge of the in-tile sweep
 constexpr int TP = TB + 2;   // LDS row stride of the tile arrays (doubles)
@@ -122,8 +77,18 @@ struct SweepSmem {
   int done[4];               // per wave: sub-tiles finished (release/acquire, workgroup scope)
 };
 
+// Staging of one 32-deep chunk of a delivery product: the left operand
+// k-major (a[k][row]), the right operand as is (b[k][col]), 128 wide.
+constexpr int KQ = 32;
+struct TaskChunk {
+  double a[KQ][2 * TB + 1];
+  double b[KQ][2 * TB + 2];
+};
 struct TaskSmem {
-  Stage64 buf[2];
+  union {
+    TaskChunk buf[2];   // 128-wide products
+    Stage64 blk[2];     // 64 x 64 products
+  };
 };
 
 union StageSmem {
@@ -140,16 +105,40 @@ __device__ __forceinline__ double load_x(const T* X, int64_t ldx, int gi, int gj
   return ok ? (double)v : 0.0;
 }
 
-// One deferred-feedback delivery (a GEMM task), 64-deep blocks double-buffered
-// through LDS: the loads of block b+1 are in flight while block b is on MFMA.
-// Task word: x = dir | overwrite << 1 | seq << 3 (seq: its place among the
-// deliveries into the same tile and direction), y = target tile row, z =
-// target tile column, w = first source | (one past last source) << 16. In
-// the persistent schedule (P) the task first waits for its source tiles and,
-// before touching the accumulator, for the deliveries ahead of it.
-template <bool P>
+// One deferred-feedback delivery (a GEMM task): out (+)= A B with A the
+// (64 nr) x K source panel and B the K x (64 nc) panel, nr, nc in {1, 2},
+// K = 64 (number of source tiles). Wave w owns the 64 x 64 output quadrant
+// (w >> 1, w & 1) as 4 x 4 MFMA blocks; quadrants outside the target are
+// skipped. 32-deep chunks go global -> registers -> LDS, double-buffered, so
+// the loads of chunk c+1 are in flight while chunk c is on MFMA; rows or
+// columns past the target are loaded from a clamped address and never used.
+// A single 64 x 64 target: the four waves split it 32 x 32 each (Acc), and
+// 64-deep blocks go global -> registers -> LDS, double-buffered.
+__device__ void run_task64(const double* Ap, int64_t lda, const double* Bp, int64_t ldb,
+                           double* out, int64_t ldo, int nb, int ow, TaskSmem& sm) {
+  Acc acc;
+  acc.zero();
+  if (!ow) acc_add_from(acc, out, ldo);
+  double ra[16], rb[16];
+  load_blk(Ap, lda, ra);
+  load_blk(Bp, ldb, rb);
+  for (int b = 0; b < nb; ++b) {
+    Stage64& st = sm.blk[b & 1];
+    put_a(st, ra);
+    put_b(st, rb);
+    __syncthreads();
+    if (b + 1 < nb) {
+      load_blk(Ap + (int64_t)(b + 1) * TB, lda, ra);
+      load_blk(Bp + (int64_t)(b + 1) * TB * ldb, ldb, rb);
+    }
+    mma_blk(acc, st);
+  }
+  acc_store(acc, out, ldo, 1.0);
+}
+
 __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
-  const int dir = tk.x & 1, ow = (tk.x >> 1) & 1, seq = tk.x >> 3;
+  const int dir = tk.x & 1, ow = (tk.x >> 1) & 1;
+  const int nr = ((tk.x >> 2) & 1) + 1, nc = ((tk.x >> 3) & 1) + 1;
   const int ti = tk.y, tj = tk.z, s0 = tk.w & 0xffff, s1 = tk.w >> 16;
   const double* Ap;
   const double* Bp;
@@ -166,43 +155,99 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
     Bp = a.U + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
     out = a.R + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
   }
-  int* cnt = a.dcnt + 2 * (ti * a.NT + tj) + dir;
-  if (P) {
-    if (threadIdx.x == 0) {
-      bool ok = true;
-      for (int s = s0; s < s1 && ok; ++s)
-        ok = poll_geq(a.tdone + (dir == 0 ? s * a.NT + tj : ti * a.NT + s), 1, a.flags);
-      if (!ok) raise_flag(a.flags, FLAG_TIMEOUT);
-    }
-    acquire_all();
-  }
   const int64_t ldb = a.np;
-  Acc acc;
-  acc.zero();
-  if (!P && !ow) acc_add_from(acc, out, a.np);
-  double ra[16], rb[16];
-  load_blk(Ap, lda, ra);
-  load_blk(Bp, ldb, rb);
-  const int nb = s1 - s0;
-  for (int b = 0; b < nb; ++b) {
-    Stage64& st = sm.buf[b & 1];
-    put_a(st, ra);
-    put_b(st, rb);
-    __syncthreads();
-    if (b + 1 < nb) {
-      load_blk(Ap + (int64_t)(b + 1) * TB, lda, ra);
-      load_blk(Bp + (int64_t)(b + 1) * TB * ldb, ldb, rb);
+  if (nr == 1 && nc == 1) {
+    run_task64(Ap, lda, Bp, ldb, out, a.np, s1 - s0, ow, sm);
+    return;
+  }
+  const int t = threadIdx.x, w = t >> 6, l = t & 63;
+  const int qr = w >> 1, qc = w & 1;
+  const bool active = qr < nr && qc < nc;
+  // per-thread load slots: A row ar, k-half ak; B k-row bk, column block bc
+  const int ar = min(t >> 1, TB * nr - 1), ak = (t & 1) * 16;
+  const int bk = t >> 3, bc = min((t & 7) * 16, TB * nc - 16);
+  const double* pa = Ap + (int64_t)ar * lda + ak;
+  const double* pb = Bp + (int64_t)bk * ldb + bc;
+  typedef double v2d __attribute__((ext_vector_type(2)));
+  v2d ra[8], rb[8];
+#define G2D_FETCH(K0_)                                                                       \
+  {                                                                                          \
+    const int64_t k0_ = (K0_);                                                               \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                          \
+      ra[i] = *reinterpret_cast<const v2d*>(pa + k0_ + 2 * i);                               \
+      rb[i] = *reinterpret_cast<const v2d*>(pb + k0_ * ldb + 2 * i);                         \
+    }                                                                                        \
+  }
+  d4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
+  const int nch = (s1 - s0) * (TB / KQ);
+  G2D_FETCH(0);
+  for (int c = 0; c < nch; ++c) {
+    TaskChunk& st = sm.buf[c & 1];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      st.a[ak + 2 * i][t >> 1] = ra[i].x;
+      st.a[ak + 2 * i + 1][t >> 1] = ra[i].y;
+      *reinterpret_cast<v2d*>(&st.b[bk][(t & 7) * 16 + 2 * i]) = rb[i];
     }
-    mma_blk(acc, st);
+    __syncthreads();
+    // every wave multiplies (a quadrant outside the target works on the
+    // clamped copies and is not stored): keeping this unconditional lets the
+    // accumulators stay in the MFMA registers across chunks. The next
+    // chunk's loads are spread over the k-steps, two per step: issued in one
+    // burst they hold up the MFMA issue
+    const bool more = c + 1 < nch;
+    const int64_t k1 = (int64_t)(c + 1) * KQ;
+    const int rb0 = TB * qr + (l & 15), cb0 = TB * qc + (l & 15);
+#pragma unroll
+    for (int kk = 0; kk < KQ / 4; ++kk) {
+      if (more) {
+        ra[kk] = *reinterpret_cast<const v2d*>(pa + k1 + 2 * kk);
+        rb[kk] = *reinterpret_cast<const v2d*>(pb + k1 * ldb + 2 * kk);
+      }
+      const int k = 4 * kk + (l >> 4);
+      double av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        av[i] = st.a[k][rb0 + 16 * i];
+        bv[i] = st.b[k][cb0 + 16 * i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[i], bv[j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
-  if (P) {
-    if (threadIdx.x == 0 && !poll_geq(cnt, seq, a.flags)) raise_flag(a.flags, FLAG_TIMEOUT);
-    acquire_all();
-    if (!ow) acc_add_from(acc, out, a.np);
+  if (active) {
+    double* o = out + (int64_t)(TB * qr) * a.np + TB * qc + (int64_t)(l >> 4) * a.np + (l & 15);
+    if (!ow) {  // every old value is requested before the first is used
+      double old[4][4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) old[i][j][r] = o[(int64_t)(16 * i + 4 * r) * a.np + 16 * j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[i][j][r] += old[i][j][r];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * a.np + 16 * j] = acc[i][j][r];
   }
-  acc_store(acc, out, a.np, 1.0);
-  if (P) publish(cnt, seq + 1);
-  else __syncthreads();
+#undef G2D_FETCH
 }
 
 // acc += A (16 x K) B (K x 16) on MFMA, both operands row-major in LDS with
@@ -391,25 +436,13 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
 // band rows 2p, 2p+1 (p = l >> 3) and sub-tile columns 2q, 2q+1 (q = l & 7):
 // eight consecutive lanes read eight different column pairs of a factor row,
 // which keeps the LDS window reads free of bank conflicts.
-template <typename T, bool P>
+template <typename T>
 __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   const int p = l >> 3, q = l & 7;
   const int br = SS * w + 2 * p;  // tile row of the lane's first row
   const int gi0 = I * TB, gj0 = J * TB;
   const T* X = (const T*)a.X;
-  if (P) {  // neighbours swept and every deferred delivery into this tile done
-    if (t == 0) {
-      const int tile = I * a.NT + J;
-      bool ok = true;
-      if (I >= 1) ok = ok && poll_geq(a.tdone + tile - a.NT, 1, a.flags);
-      if (J >= 1) ok = ok && poll_geq(a.tdone + tile - 1, 1, a.flags);
-      ok = ok && poll_geq(a.dcnt + 2 * tile, a.expect[2 * tile], a.flags);
-      ok = ok && poll_geq(a.dcnt + 2 * tile + 1, a.expect[2 * tile + 1], a.flags);
-      if (!ok) raise_flag(a.flags, FLAG_TIMEOUT);
-    }
-    acquire_all();
-  }
 
   // every global load of the prologue is issued before any is used
   double lv[16], uv[16], ga[16], gb[16];
@@ -551,7 +584,6 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   if (l == 0) sm.red[w] = part;
   __syncthreads();
   if (t == 0) a.objp[I * a.NT + J] = (sm.red[0] + sm.red[1]) + (sm.red[2] + sm.red[3]);
-  if (P) publish(a.tdone + I * a.NT + J, 1);
 }
 
 template <typename T>
@@ -560,43 +592,10 @@ __global__ __launch_bounds__(NT) void k_stage(StageArgs a) {
   const int b = blockIdx.x;
   if (b < a.nsweep) {
     const int I = a.ilo + b;
-    run_sweep<T, false>(a, I, a.stage - I, sm.s);
+    run_sweep<T>(a, I, a.stage - I, sm.s);
   } else {
-    run_task<false>(a, a.tasks[b - a.nsweep], sm.t);
+    run_task(a, a.tasks[b - a.nsweep], sm.t);
   }
-}
-
-// The whole sweep as one persistent launch: every workgroup takes the next
-// item of the work list (tile sweeps and deliveries in the order of the tile
-// anti-diagonals) until the list is exhausted. An item only waits for items
-// ahead of it in the list, and items are taken in list order, so the
-// earliest unfinished item always belongs to a running workgroup and can
-// proceed.
-template <typename T>
-__global__ __launch_bounds__(NT) void k_persist(StageArgs a) {
-  __shared__ StageSmem sm;
-  __shared__ int cur;
-  for (;;) {
-    if (threadIdx.x == 0) cur = atomicAdd(a.next, 1);
-    __syncthreads();
-    // the cursor must be a scalar: with a per-lane value the loop exit is
-    // divergent, and the compiler may then split the workgroup's lanes
-    // across iterations of a loop that contains barriers
-    const int idx = __builtin_amdgcn_readfirstlane(cur);
-    __syncthreads();
-    if (idx >= a.nitems) break;
-    const int4 it = a.items[idx];
-    if (it.x & 4) run_sweep<T, true>(a, it.y, it.z, sm.s);
-    else run_task<true>(a, it, sm.t);
-    // keeps the item's closing thread-0 store and the next cursor update in
-    // separate barrier intervals, so the two single-lane regions are never
-    // merged across the loop's back edge
-    __syncthreads();
-  }
-}
-
-__global__ void k_zero_ints(int* p, int n) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
 __global__ __launch_bounds__(NT) void k_obj_reduce(const double* part, int count, double* out) {
@@ -622,12 +621,9 @@ __global__ void k_zero_flags(int* p) {
 
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
-static int sync_ints(const Factors& f) { return 64 + 3 * f.MT * f.NT; }
-
 size_t workspace_bytes(const Factors& f) {
   const size_t tile = (size_t)f.mp * f.np * sizeof(double);
-  return 256 + align256((size_t)f.MT * f.NT * sizeof(double)) + 4 * tile +
-         align256((size_t)sync_ints(f) * sizeof(int));
+  return 256 + align256((size_t)f.MT * f.NT * sizeof(double)) + 4 * tile;
 }
 
 Workspace workspace_carve(const Factors& f, void* base) {
@@ -642,47 +638,87 @@ Workspace workspace_carve(const Factors& f, void* base) {
   w.R = (double*)(p + tile);
   w.E = (double*)(p + 2 * tile);
   w.C = (double*)(p + 3 * tile);
-  w.sync = (int*)(p + 4 * tile);
-  w.nsync = sync_ints(f);
   return w;
 }
 
+// Delivery plan of the deferred feedback. Targets are grouped in 2 x 2
+// super-tiles (fewer at an odd edge); for super-tile rows {2a, 2a+1} and
+// columns {2b, 2b+1} the down direction gets
+//   - source tile rows 0 .. 2a-4 in batches of g, as products onto the whole
+//     super-tile (up to 128 x 128), each in a launch after its sources are
+//     swept and at least two launches before the super-tile's first sweep;
+//   - source rows 2a-3 .. 2a-2 onto rows 2a, 2a+1 of one tile column c at a
+//     time, in launch 2a + c - 1 (the last before tile (2a, c) is swept);
+//   - source row 2a-1 onto tile (2a+1, c), in launch 2a + c;
+// (source row 2a-1 of tile (2a, c) and 2a of tile (2a+1, c) are the sweeping
+// workgroup's own neighbour products). The right direction is the same with
+// rows and columns exchanged. Every target gets each source once, at most one
+// delivery per launch, the first one overwriting.
+// Task word: x = dir | overwrite << 1 | (rows - 1) << 2 | (cols - 1) << 3
+// (rows, cols in tiles), y = first target tile row, z = first target tile
+// column, w = first source | (one past the last source) << 16.
 void schedule_tasks(int MT, int NTt, int g, std::vector<int4>& all, std::vector<int>& off) {
   const int S = MT + NTt - 1;
   if (g < 1) g = 1;
   std::vector<std::vector<int4>> per(S);
-  for (int ti = 0; ti < MT; ++ti) {
-    for (int tj = 0; tj < NTt; ++tj) {
-      const int sig = ti + tj;
-      if (sig < 2) continue;
+  auto emit = [&](int launch, int dir, int ow, int ti, int tj, int nr, int nc, int s0, int s1) {
+    per[launch].push_back(make_int4(dir | (ow << 1) | ((nr - 1) << 2) | ((nc - 1) << 3), ti, tj,
+                                    s0 | (s1 << 16)));
+  };
+  for (int a = 0; 2 * a < MT; ++a) {
+    for (int b = 0; 2 * b < NTt; ++b) {
+      const int r0 = 2 * a, c0 = 2 * b;
+      const int nr = std::min(2, MT - r0), nc = std::min(2, NTt - c0);
       for (int dir = 0; dir < 2; ++dir) {
-        const int fixed = dir == 0 ? tj : ti;  // source stage = source index + fixed
-        const int lim = dir == 0 ? ti - 2 : tj - 2;
-        if (lim < 0) continue;
+        // along: the target index that sources run along (rows for down)
+        const int t0 = dir == 0 ? r0 : c0, nt = dir == 0 ? nr : nc;
+        const int o0 = dir == 0 ? c0 : r0, no = dir == 0 ? nc : nr;  // the other index
         bool first = true;
-        auto add = [&](int launch, int lo, int hi) {
-          const int s0 = std::max(lo - fixed, 0), s1 = std::min(hi - fixed, lim) + 1;
-          if (s1 <= s0) return;
-          const int ow = first ? 1 : 0;
-          first = false;
-          per[launch].push_back(make_int4(dir | (ow << 1), ti, tj, s0 | (s1 << 16)));
-        };
-        // whole batches of g source anti-diagonals, spread over the g launches
-        // after the batch completes, each at least one launch before the target
-        for (int beta = 0; (beta + 1) * g <= sig - 2; ++beta) {
-          const int launch = (beta + 1) * g + ((sig - (beta + 1) * g - 2) % g);
-          add(launch, beta * g, beta * g + g - 1);
+        // far sources 0 .. t0-4, batched: each batch in a launch after its
+        // sources are swept (spread by the super-tile index), then pulled
+        // earlier where needed so that no two batches share a launch
+        const int far = t0 - 4;
+        const int latest = r0 + c0 - 2;  // two launches before the first sweep
+        std::vector<int> bl;
+        for (int beta = 0; beta * g <= far; ++beta) {
+          const int sl = std::min(far, beta * g + g - 1);
+          bl.push_back(std::min(latest, sl + o0 + no + (a + b) % g));
         }
-        // the rest, in the launch just before the target is swept
-        add(sig - 1, g * ((sig - 2) / g), sig - 2);
+        for (int i = (int)bl.size() - 2; i >= 0; --i) bl[i] = std::min(bl[i], bl[i + 1] - 1);
+        for (int beta = 0; beta < (int)bl.size(); ++beta) {
+          const int s0 = beta * g, sl = std::min(far, s0 + g - 1);
+          emit(bl[beta], dir, first, r0, c0, nr, nc, s0, sl + 1);
+          first = false;
+        }
+        // near sources t0-3 .. t0-2 onto both targets along, one other index at a time
+        if (t0 - 2 >= 0) {
+          const int s0 = std::max(0, t0 - 3);
+          for (int o = o0; o < o0 + no; ++o) {
+            const int launch = t0 + o - 1;
+            if (dir == 0) emit(launch, 0, first, r0, o, nt, 1, s0, t0 - 1);
+            else emit(launch, 1, first, o, c0, 1, nt, s0, t0 - 1);
+          }
+          first = false;
+        }
+        // source t0-1 onto the second target along only
+        if (nt == 2 && t0 - 1 >= 0) {
+          for (int o = o0; o < o0 + no; ++o) {
+            const int launch = t0 + o;
+            if (dir == 0) emit(launch, 0, first, r0 + 1, o, 1, 1, t0 - 1, t0);
+            else emit(launch, 1, first, o, c0 + 1, 1, 1, t0 - 1, t0);
+          }
+        }
       }
     }
   }
   all.clear();
   off.assign(S + 1, 0);
   for (int k = 0; k < S; ++k) {
+    // biggest products first, so the short ones fill in behind them
     std::stable_sort(per[k].begin(), per[k].end(), [](const int4& x, const int4& y) {
-      return ((x.w >> 16) - (x.w & 0xffff)) > ((y.w >> 16) - (y.w & 0xffff));
+      const int wx = ((x.w >> 16) - (x.w & 0xffff)) * (((x.x >> 2) & 1) + 1) * (((x.x >> 3) & 1) + 1);
+      const int wy = ((y.w >> 16) - (y.w & 0xffff)) * (((y.x >> 2) & 1) + 1) * (((y.x >> 3) & 1) + 1);
+      return wx > wy;
     });
     off[k] = (int)all.size();
     all.insert(all.end(), per[k].begin(), per[k].end());
@@ -692,57 +728,25 @@ void schedule_tasks(int MT, int NTt, int g, std::vector<int4>& all, std::vector<
 
 void free_schedule(Schedule& sc) {
   if (sc.d_tasks) (void)hipFree(sc.d_tasks);
-  if (sc.d_items) (void)hipFree(sc.d_items);
-  if (sc.d_expect) (void)hipFree(sc.d_expect);
   sc.d_tasks = nullptr;
-  sc.d_items = nullptr;
-  sc.d_expect = nullptr;
 }
 
-template <typename V>
-static gptq2d_status upload(V** dst, const std::vector<V>& v, const char* what) {
-  if (v.empty()) return GPTQ2D_OK;
-  hipError_t e = hipMalloc(dst, v.size() * sizeof(V));
-  if (e != hipSuccess) return hip_fail(e, what);
-  e = hipMemcpy(*dst, v.data(), v.size() * sizeof(V), hipMemcpyHostToDevice);
-  if (e != hipSuccess) return hip_fail(e, what);
-  return GPTQ2D_OK;
-}
-
-gptq2d_status build_schedule(Factors& f, int g, bool persist) {
+gptq2d_status build_schedule(Factors& f, int g) {
   std::vector<int4> all;
   std::vector<int> off;
   if (g < 1) g = 1;
   schedule_tasks(f.MT, f.NT, g, all, off);
   free_schedule(f.sched);
-  const int S = f.MT + f.NT - 1;
-  // the work list of the persistent form: per tile anti-diagonal k, its
-  // sweeps, then the tasks of launch k; seq numbers the deliveries into
-  // each (tile, direction) in list order
-  std::vector<int4> items;
-  std::vector<int> expect((size_t)2 * f.MT * f.NT, 0);
-  for (int k = 0; k < S; ++k) {
-    const int ilo = std::max(0, k - (f.NT - 1)), ihi = std::min(k, f.MT - 1);
-    for (int I = ilo; I <= ihi; ++I) items.push_back(make_int4(4, I, k - I, 0));
-    for (int i = off[k]; i < off[k + 1]; ++i) {
-      int4 tk = all[i];
-      int& cnt = expect[2 * (tk.y * f.NT + tk.z) + (tk.x & 1)];
-      tk.x = (tk.x & 3) | (cnt << 3);
-      all[i].x = tk.x;
-      ++cnt;
-      items.push_back(tk);
-    }
+  if (!all.empty()) {
+    hipError_t e = hipMalloc(&f.sched.d_tasks, all.size() * sizeof(int4));
+    if (e != hipSuccess) return hip_fail(e, "schedule allocation");
+    e = hipMemcpy(f.sched.d_tasks, all.data(), all.size() * sizeof(int4), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "schedule upload");
   }
-  gptq2d_status st = upload(&f.sched.d_tasks, all, "schedule upload");
-  if (st == GPTQ2D_OK && persist) st = upload(&f.sched.d_items, items, "work list upload");
-  if (st == GPTQ2D_OK && persist) st = upload(&f.sched.d_expect, expect, "work list upload");
-  if (st != GPTQ2D_OK) return st;
   f.sched.g = g;
-  f.sched.stages = S;
+  f.sched.stages = f.MT + f.NT - 1;
   f.sched.offset = off;
   f.sched.ntasks = all.size();
-  f.sched.persist = persist;
-  f.sched.nitems = (int)items.size();
   return GPTQ2D_OK;
 }
 
@@ -775,22 +779,7 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
   a.flags = ws.flags;
   hipLaunchKernelGGL(k_zero_flags, dim3(1), dim3(64), 0, s, ws.flags);
   const Schedule& S = f.sched;
-  if (S.persist) {
-    a.items = S.d_items;
-    a.nitems = S.nitems;
-    a.next = ws.sync;
-    a.tdone = ws.sync + 64;
-    a.dcnt = ws.sync + 64 + f.MT * f.NT;
-    a.expect = S.d_expect;
-    hipLaunchKernelGGL(k_zero_ints, dim3(64), dim3(256), 0, s, ws.sync, ws.nsync);
-    int per_cu = 0, cus = 0, dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_persist<T>, NT, 0);
-    if (e != hipSuccess) return hip_fail(e, "occupancy query");
-    const int grid = std::max(1, std::min(S.nitems, std::max(per_cu, 1) * cus));
-    hipLaunchKernelGGL(k_persist<T>, dim3(grid), dim3(NT), 0, s, a);
-  } else for (int k = 0; k < S.stages; ++k) {
+  for (int k = 0; k < S.stages; ++k) {
     const int ilo = std::max(0, k - (f.NT - 1)), ihi = std::min(k, f.MT - 1);
     a.stage = k;
     a.ilo = ilo;

@@ -45,6 +45,10 @@ def test_null_handle_is_rejected(lib):
     lib.gptq2d_factors_destroy(null)
 
 
+def _task_fields(x):
+    return x & 1, (x >> 1) & 1, ((x >> 2) & 1) + 1, ((x >> 3) & 1) + 1
+
+
 def _check_plan(m, n, g):
     tasks, offs = binding.gptq2d_schedule_tasks(m, n, g)
     MT, NT = (m + 63) // 64, (n + 63) // 64
@@ -55,16 +59,20 @@ def _check_plan(m, n, g):
     for k in range(S):
         seen = set()
         for x, ti, tj, w in tasks[offs[k]:offs[k + 1]]:
-            d, ow = x & 1, (x >> 1) & 1
+            d, ow, nr, nc = _task_fields(x)
             s0, s1 = w & 0xFFFF, w >> 16
-            assert 0 <= ti < MT and 0 <= tj < NT and s0 < s1
-            assert ti + tj >= k + 1, "delivered after the target was swept"
-            key = (d, ti, tj)
-            assert key not in seen, "two tasks of one launch write the same buffer"
-            seen.add(key)
-            fixed = tj if d == 0 else ti
-            assert (s1 - 1) + fixed <= k - 1, "a source is not finished before the launch"
-            got.setdefault(key, []).append((k, s0, s1, ow))
+            assert 0 <= ti and ti + nr <= MT and 0 <= tj and tj + nc <= NT and s0 < s1
+            for r in range(nr):
+                for c in range(nc):
+                    I, J = ti + r, tj + c
+                    assert I + J >= k + 1, "delivered after the target was swept"
+                    key = (d, I, J)
+                    assert key not in seen, "two tasks of one launch write the same buffer"
+                    seen.add(key)
+                    # the sources of this target: tiles (s, J) or (I, s)
+                    fixed = J if d == 0 else I
+                    assert (s1 - 1) + fixed <= k - 1, "a source is not finished before the launch"
+                    got.setdefault(key, []).append((k, s0, s1, ow))
     # every target receives every source except its immediate predecessor,
     # exactly once, and the first delivery overwrites
     for ti, tj in itertools.product(range(MT), range(NT)):
@@ -74,15 +82,14 @@ def _check_plan(m, n, g):
             if lim < 0:
                 assert not lst
                 continue
-            cover = sorted((s0, s1) for _, s0, s1, _ in lst)
+            lst.sort()
             pos = 0
-            for s0, s1 in cover:
+            for _, s0, s1, _ in sorted(lst, key=lambda e: e[1]):
                 assert s0 == pos
                 pos = s1
             assert pos == lim + 1
-            lst.sort()
             assert [ow for *_, ow in lst] == [1] + [0] * (len(lst) - 1)
-            assert max(r - l for _, l, r, _ in lst) <= g
+            assert max(r - l for _, l, r, _ in lst) <= max(g, 2)
 
 
 @pytest.mark.parametrize("m,n", [(1, 1), (64, 64), (65, 200), (512, 384), (700, 130), (2048, 64)])

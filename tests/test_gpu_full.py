@@ -4,7 +4,7 @@ At these sizes the oracle cannot replay a whole sweep in test time, so each
 run is judged on what the oracle can compute exactly and on properties that
 hold at any size:
 
-- the leading 2048 x 2048 block of the sweep is self-contained (an entry only
+- the leading 1280 x 1280 block of the sweep is self-contained (an entry only
   depends on entries above and to the left of it), so the oracle replays that
   corner with the GPU's own factors and the GPU's Z as hints, under the same
   window rule as the small cases;
@@ -25,7 +25,7 @@ import parity as pr
 
 pytestmark = pytest.mark.gpu
 
-CORNER = 2048
+CORNER = 1280
 
 
 def _factor_residual(M, F, lam, left, nprobe=3, seed=1):

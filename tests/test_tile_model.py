@@ -16,7 +16,8 @@ def _lib():
 
 
 @pytest.mark.parametrize("m,n,g", [(40, 30, 4), (64, 64, 1), (150, 130, 1), (150, 130, 3),
-                                   (200, 70, 2), (65, 260, 4)])
+                                   (200, 70, 2), (65, 260, 4), (400, 330, 2), (330, 460, 1),
+                                   (520, 200, 3)])
 def test_tile_model_matches_oracle(m, n, g):
     X, A, B = wl.random_problem(m, n, 3, "f64", "wishart").widened()
     L, _, U, _ = oracle.factors(A, B)

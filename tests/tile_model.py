@@ -38,13 +38,16 @@ def tile_model_round(X, L, U, g=4):
     for k in range(MT + NT - 1):
         for x, ti, tj, w in tasks[offs[k]:offs[k + 1]]:
             d, ow = x & 1, (x >> 1) & 1
+            nr, nc = ((x >> 2) & 1) + 1, ((x >> 3) & 1) + 1
             src = slice((w & 0xFFFF) * T, (w >> 16) * T)
+            rows = slice(ti * T, (ti + nr) * T)
+            cols = slice(tj * T, (tj + nc) * T)
             if d == 0:
-                v = Lp[blk(ti), src] @ E[src, blk(tj)]
-                P[blk(ti), blk(tj)] = v if ow else P[blk(ti), blk(tj)] + v
+                v = Lp[rows, src] @ E[src, cols]
+                P[rows, cols] = v if ow else P[rows, cols] + v
             else:
-                v = C[blk(ti), src] @ Up[src, blk(tj)]
-                R[blk(ti), blk(tj)] = v if ow else R[blk(ti), blk(tj)] + v
+                v = C[rows, src] @ Up[src, cols]
+                R[rows, cols] = v if ow else R[rows, cols] + v
         for I in range(max(0, k - NT + 1), min(k, MT - 1) + 1):
             J = k - I
             Dn = np.zeros((T, T))
