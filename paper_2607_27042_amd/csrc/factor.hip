@@ -17,6 +17,8 @@
 // MFMA) and a right-looking blocked triangular inverse (MFMA).
 #include <math.h>
 
+#include <algorithm>
+
 #include "device.hpp"
 #include "internal.hpp"
 
@@ -402,51 +404,96 @@ __global__ __launch_bounds__(NT) void k_panel(FacArgs f, int kb) {
 }
 
 // ---------------------------------------------------------------------------
-// Update step kb, both sides in one grid:
-//   Q[bi][bj] -= Lc[bi][kb] Lc[bj][kb]^T          (kb < bj <= bi)
-//   S[ib][jb] += Lc[ib][kb] Li[kb][jb]            (ib > kb, jb <= kb; kb == jb overwrites)
+// Update with the finished panels k0 .. k1-1 (both sides in one grid):
+//   Q[bi][bj] -= sum_kb Lc[bi][kb] Lc[bj][kb]^T      (qa <= bj < qb, bj <= bi)
+//   S[ib][jb] += sum_kb Lc[ib][kb] Li[kb][jb]        (sa <= ib < sb, jb < k1,
+//                                                      max(k0, jb) <= kb < k1)
+// S is the running sum of the triangular inverse, kept in place in Li; its
+// first contribution (kb = jb) overwrites. Called with one panel for the
+// columns / rows still inside the current group of panels, and with the
+// whole group for everything beyond it, so the bulk of the trailing work is
+// done with 256-deep products.
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ int update_count(const Side& sd, int kb) {
-  if (kb >= sd.nb) return 0;
-  const int rest = sd.nb - kb - 1;
-  return rest * (rest + 1) / 2 + rest * (kb + 1);
+struct UpdRange {
+  int qa, qb, sa, sb, k0, k1;
+};
+
+__device__ __forceinline__ void upd_counts(const Side& sd, const UpdRange& r, int& nq, int& ns) {
+  nq = ns = 0;
+  if (r.k0 >= sd.nb) return;
+  for (int bj = r.qa; bj < min(r.qb, sd.nb); ++bj) nq += sd.nb - bj;
+  ns = max(0, min(r.sb, sd.nb) - r.sa) * min(r.k1, sd.nb);
 }
 
-__global__ __launch_bounds__(NT) void k_update(FacArgs f, int kb) {
-  __shared__ Stage64 st;
+// acc += sum over 64-deep blocks b of A_b op(B_b), A_b at pa + b*sa_, B_b at
+// pb + b*sb_; BT: B given transposed. Double-buffered through LDS.
+template <int BT>
+__device__ void gemm_blocks(Acc& acc, const double* pa, int64_t lda, int64_t sa_, const double* pb,
+                            int64_t ldb, int64_t sb_, int nb, Stage64* st) {
+  double ra[16], rb[16];
+  load_blk(pa, lda, ra);
+  load_blk(pb, ldb, rb);
+  for (int b = 0; b < nb; ++b) {
+    Stage64& s = st[b & 1];
+    put_a(s, ra);
+    if (BT) put_bt(s, rb);
+    else put_b(s, rb);
+    __syncthreads();
+    if (b + 1 < nb) {
+      load_blk(pa + (b + 1) * sa_, lda, ra);
+      load_blk(pb + (b + 1) * sb_, ldb, rb);
+    }
+    mma_blk(acc, s);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_update(FacArgs f, UpdRange r) {
+  __shared__ Stage64 st[2];
   int b = blockIdx.x;
-  const int n0 = update_count(f.s[0], kb);
-  const Side& sd = (b < n0) ? f.s[0] : f.s[1];
-  if (b >= n0) b -= n0;
-  const int rest = sd.nb - kb - 1;
-  const int nsyrk = rest * (rest + 1) / 2;
+  int nq0, ns0;
+  upd_counts(f.s[0], r, nq0, ns0);
+  const bool s1 = b >= nq0 + ns0;
+  const Side& sd = s1 ? f.s[1] : f.s[0];
+  if (s1) b -= nq0 + ns0;
+  int nq, ns;
+  upd_counts(sd, r, nq, ns);
+  const int k1 = min(r.k1, sd.nb);
   Acc acc;
   acc.zero();
-  if (b < nsyrk) {
-    int bi, bj;
-    tri_index(b, bi, bj);
-    bi += kb + 1;
-    bj += kb + 1;
-    gemm64<1>(acc, sd.gr + (int64_t)bi * TB * sd.dp + (int64_t)kb * TB, sd.dp,
-              sd.gr + (int64_t)bj * TB * sd.dp + (int64_t)kb * TB, sd.dp, st);
+  if (b < nq) {
+    int bj = r.qa;
+    while (b >= sd.nb - bj) {
+      b -= sd.nb - bj;
+      ++bj;
+    }
+    const int bi = bj + b;
+    gemm_blocks<1>(acc, sd.gr + (int64_t)bi * TB * sd.dp + (int64_t)r.k0 * TB, sd.dp, TB,
+                   sd.gr + (int64_t)bj * TB * sd.dp + (int64_t)r.k0 * TB, sd.dp, TB, k1 - r.k0, st);
     double* out = sd.gr + (int64_t)bi * TB * sd.dp + (int64_t)bj * TB;
+    double old[2][2][4];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int v = 0; v < 2; ++v)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          double* q = out + (int64_t)acc_row(u, r) * sd.dp + acc_col(v);
-          *q = *q - acc.t[2 * u + v][r];
-        }
+        for (int q = 0; q < 4; ++q) old[u][v][q] = out[(int64_t)acc_row(u, q) * sd.dp + acc_col(v)];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int v = 0; v < 2; ++v)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          out[(int64_t)acc_row(u, q) * sd.dp + acc_col(v)] = old[u][v][q] - acc.t[2 * u + v][q];
   } else {
-    b -= nsyrk;
-    const int w = kb + 1, ib = kb + 1 + b / w, jb = b % w;
+    b -= nq;
+    const int ib = r.sa + b / k1, jb = b % k1;
+    const int kb0 = max(r.k0, jb);
     double* out = sd.li + (int64_t)ib * TB * sd.dp + (int64_t)jb * TB;
-    if (jb != kb) acc_add_from(acc, out, sd.dp);
-    gemm64<0>(acc, sd.gr + (int64_t)ib * TB * sd.dp + (int64_t)kb * TB, sd.dp,
-              sd.li + (int64_t)kb * TB * sd.dp + (int64_t)jb * TB, sd.dp, st);
+    if (jb < r.k0) acc_add_from(acc, out, sd.dp);
+    gemm_blocks<0>(acc, sd.gr + (int64_t)ib * TB * sd.dp + (int64_t)kb0 * TB, sd.dp, TB,
+                   sd.li + (int64_t)kb0 * TB * sd.dp + (int64_t)jb * TB, sd.dp, (int64_t)TB * sd.dp,
+                   k1 - kb0, st);
     acc_store(acc, out, sd.dp, 1.0);
   }
 }
@@ -558,10 +605,11 @@ static FacArgs fac_args(Factors& f) {
 }
 
 static int h_panel_count(int nb, int kb) { return kb < nb ? nb : 0; }
-static int h_update_count(int nb, int kb) {
-  if (kb >= nb) return 0;
-  const int rest = nb - kb - 1;
-  return rest * (rest + 1) / 2 + rest * (kb + 1);
+static int h_upd_count(int nb, const UpdRange& r) {
+  if (r.k0 >= nb) return 0;
+  int nq = 0;
+  for (int bj = r.qa; bj < std::min(r.qb, nb); ++bj) nq += nb - bj;
+  return nq + std::max(0, std::min(r.sb, nb) - r.sa) * std::min(r.k1, nb);
 }
 
 gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t lda,
@@ -576,12 +624,20 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
   else
     hipLaunchKernelGGL(k_gram<double>, dim3(tri), dim3(NT), 0, s, a, (const double*)A, lda,
                        (const double*)B, ldb);
-  for (int kb = 0; kb < nbmax; ++kb) {
-    hipLaunchKernelGGL(k_diag, dim3(2), dim3(NT), 0, s, a, kb);
-    const int np_ = h_panel_count(nb0, kb) + h_panel_count(nb1, kb);
-    if (np_ > 0) hipLaunchKernelGGL(k_panel, dim3(np_), dim3(NT), 0, s, a, kb);
-    const int nu = h_update_count(nb0, kb) + h_update_count(nb1, kb);
-    if (nu > 0) hipLaunchKernelGGL(k_update, dim3(nu), dim3(NT), 0, s, a, kb);
+  auto update = [&](const UpdRange& r) {
+    const int nu = h_upd_count(nb0, r) + h_upd_count(nb1, r);
+    if (nu > 0) hipLaunchKernelGGL(k_update, dim3(nu), dim3(NT), 0, s, a, r);
+  };
+  constexpr int GROUP = 4;  // panels per group: 256-deep trailing products
+  for (int g0 = 0; g0 < nbmax; g0 += GROUP) {
+    const int g1 = std::min(g0 + GROUP, nbmax);
+    for (int kb = g0; kb < g1; ++kb) {
+      hipLaunchKernelGGL(k_diag, dim3(2), dim3(NT), 0, s, a, kb);
+      const int np_ = h_panel_count(nb0, kb) + h_panel_count(nb1, kb);
+      if (np_ > 0) hipLaunchKernelGGL(k_panel, dim3(np_), dim3(NT), 0, s, a, kb);
+      if (kb + 1 < g1) update(UpdRange{kb + 1, g1, kb + 1, g1, kb, kb + 1});
+    }
+    update(UpdRange{g1, nbmax, g1, nbmax, g0, g1});
   }
   hipLaunchKernelGGL(k_finalize, dim3(tri), dim3(NT), 0, s, a);
   return check_launch("factorisation launch");
