@@ -33,6 +33,11 @@ static int round_up(int v, int a) { return (v + a - 1) / a * a; }
 static void free_all(Factors* f) {
   for (void* p : f->allocations) (void)hipFree(p);
   f->allocations.clear();
+  if (f->ev_near) (void)hipEventDestroy(f->ev_near);
+  if (f->ev_far) (void)hipEventDestroy(f->ev_far);
+  if (f->aux) (void)hipStreamDestroy(f->aux);
+  f->ev_near = f->ev_far = nullptr;
+  f->aux = nullptr;
   free_schedule(f->sched);
 }
 
@@ -106,6 +111,12 @@ gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
       he = hipMemset(f->flags, 0, 256);
       if (he != hipSuccess) st = hip_fail(he, "hipMemset");
     }
+  }
+  if (st == GPTQ2D_OK) {
+    he = hipStreamCreateWithFlags(&f->aux, hipStreamNonBlocking);
+    if (he == hipSuccess) he = hipEventCreateWithFlags(&f->ev_near, hipEventDisableTiming);
+    if (he == hipSuccess) he = hipEventCreateWithFlags(&f->ev_far, hipEventDisableTiming);
+    if (he != hipSuccess) st = hip_fail(he, "stream / event creation");
   }
   if (st == GPTQ2D_OK)
     st = build_schedule(*f, env_int("GPTQ2D_BATCH", 4));

@@ -624,20 +624,47 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
   else
     hipLaunchKernelGGL(k_gram<double>, dim3(tri), dim3(NT), 0, s, a, (const double*)A, lda,
                        (const double*)B, ldb);
-  auto update = [&](const UpdRange& r) {
+  auto update = [&](const UpdRange& r, hipStream_t st) {
     const int nu = h_upd_count(nb0, r) + h_upd_count(nb1, r);
-    if (nu > 0) hipLaunchKernelGGL(k_update, dim3(nu), dim3(NT), 0, s, a, r);
+    if (nu > 0) hipLaunchKernelGGL(k_update, dim3(nu), dim3(NT), 0, st, a, r);
   };
-  constexpr int GROUP = 4;  // panels per group: 256-deep trailing products
+  // Groups of four panels. Inside a group each panel updates only the
+  // group's remaining columns (and rows of the inverse sum); afterwards the
+  // whole group updates everything beyond it with 256-deep products: the
+  // next group's four columns on the caller's stream (they are needed
+  // first), the rest on the second stream, where it overlaps the next
+  // group's diagonal blocks and panels. Before touching tiles that the far
+  // part writes, the caller's stream waits for it.
+  constexpr int GROUP = 4;
+  hipError_t he = hipSuccess;
+  bool far_pending = false;
   for (int g0 = 0; g0 < nbmax; g0 += GROUP) {
-    const int g1 = std::min(g0 + GROUP, nbmax);
+    const int g1 = std::min(g0 + GROUP, nbmax), g2 = std::min(g1 + GROUP, nbmax);
     for (int kb = g0; kb < g1; ++kb) {
       hipLaunchKernelGGL(k_diag, dim3(2), dim3(NT), 0, s, a, kb);
       const int np_ = h_panel_count(nb0, kb) + h_panel_count(nb1, kb);
       if (np_ > 0) hipLaunchKernelGGL(k_panel, dim3(np_), dim3(NT), 0, s, a, kb);
-      if (kb + 1 < g1) update(UpdRange{kb + 1, g1, kb + 1, g1, kb, kb + 1});
+      if (kb + 1 < g1) update(UpdRange{kb + 1, g1, kb + 1, g1, kb, kb + 1}, s);
     }
-    update(UpdRange{g1, nbmax, g1, nbmax, g0, g1});
+    if (far_pending) {
+      he = hipStreamWaitEvent(s, f.ev_far, 0);
+      if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
+      far_pending = false;
+    }
+    update(UpdRange{g1, g2, g1, g2, g0, g1}, s);
+    if (g2 < nbmax) {
+      he = hipEventRecord(f.ev_near, s);
+      if (he == hipSuccess) he = hipStreamWaitEvent(f.aux, f.ev_near, 0);
+      if (he != hipSuccess) return hip_fail(he, "event record / wait");
+      update(UpdRange{g2, nbmax, g2, nbmax, g0, g1}, f.aux);
+      he = hipEventRecord(f.ev_far, f.aux);
+      if (he != hipSuccess) return hip_fail(he, "hipEventRecord");
+      far_pending = true;
+    }
+  }
+  if (far_pending) {
+    he = hipStreamWaitEvent(s, f.ev_far, 0);
+    if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
   }
   hipLaunchKernelGGL(k_finalize, dim3(tri), dim3(NT), 0, s, a);
   return check_launch("factorisation launch");

@@ -39,6 +39,10 @@ struct Factors {
   double* inv[2] = {nullptr, nullptr};   // inverse of that Cholesky factor
   double* dinv[2] = {nullptr, nullptr};  // inverses of its 64 x 64 diagonal blocks
   int* flags = nullptr;                  // device error bits of the factorisation
+  // second stream of the factorisation: the far part of each group's
+  // trailing update runs there, next to the following group's panels
+  hipStream_t aux = nullptr;
+  hipEvent_t ev_near = nullptr, ev_far = nullptr;
   Schedule sched;
   std::vector<void*> allocations;
 };
