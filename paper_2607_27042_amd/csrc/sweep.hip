@@ -24,6 +24,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <queue>
 #include <vector>
 
 #include "device.hpp"
@@ -77,11 +78,15 @@ struct SweepSmem {
   int done[4];               // per wave: sub-tiles finished (release/acquire, workgroup scope)
 };
 
-// Staging of one 32-deep chunk of a delivery product: the left operand
-// k-major (a[k][row]), the right operand as is (b[k][col]), 128 wide.
+// Staging of one 32-deep chunk of a delivery product, filled by direct
+// global -> LDS loads (each wave instruction moves 64 lanes x 16 bytes to 1 KB
+// of consecutive LDS): the left operand as a[kp][row][e] = A[row][2 kp + e]
+// (128 rows, so each 1 KB block holds one k-pair of 64 rows), the right
+// operand as rows b[k][col] padded to 130 doubles. Both layouts make an MFMA
+// operand read take the minimum two LDS passes.
 constexpr int KQ = 32;
 struct TaskChunk {
-  double a[KQ][2 * TB + 1];
+  double a[KQ / 2][2 * TB][2];
   double b[KQ][2 * TB + 2];
 };
 struct TaskSmem {
@@ -163,20 +168,25 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   const int qr = w >> 1, qc = w & 1;
   const bool active = qr < nr && qc < nc;
-  // per-thread load slots: A row ar, k-half ak; B k-row bk, column block bc
-  const int ar = min(t >> 1, TB * nr - 1), ak = (t & 1) * 16;
-  const int bk = t >> 3, bc = min((t & 7) * 16, TB * nc - 16);
-  const double* pa = Ap + (int64_t)ar * lda + ak;
-  const double* pb = Bp + (int64_t)bk * ldb + bc;
-  typedef double v2d __attribute__((ext_vector_type(2)));
-  v2d ra[8], rb[8];
-#define G2D_FETCH(K0_)                                                                       \
-  {                                                                                          \
-    const int64_t k0_ = (K0_);                                                               \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                          \
-      ra[i] = *reinterpret_cast<const v2d*>(pa + k0_ + 2 * i);                               \
-      rb[i] = *reinterpret_cast<const v2d*>(pb + k0_ * ldb + 2 * i);                         \
-    }                                                                                        \
+  typedef __attribute__((address_space(3))) void lds_void;
+  // this lane's source rows / columns (clamped to the target)
+  const double* pa0 = Ap + (int64_t)min(l, TB * nr - 1) * lda;          // A row l (first half)
+  const double* pa1 = Ap + (int64_t)min(TB + l, TB * nr - 1) * lda;     // A row 64 + l
+  const double* pb0 = Bp + min(2 * l, TB * nc - 2);                      // B columns 2l, 2l+1
+  // wave w moves A blocks j = w + 4i (k-pair j >> 1, row half j & 1) and B
+  // rows k = w + 4i, i = 0..7
+#define G2D_ISSUE(C_)                                                                          \
+  {                                                                                            \
+    TaskChunk& d_ = sm.buf[(C_) & 1];                                                          \
+    const int64_t k0_ = (int64_t)(C_) * KQ;                                                    \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                            \
+      const int j = w + 4 * i, kp = j >> 1, hf = j & 1;                                        \
+      __builtin_amdgcn_global_load_lds((const void*)((hf ? pa1 : pa0) + k0_ + 2 * kp),         \
+                                       (lds_void*)&d_.a[kp][TB * hf][0], 16, 0, 0);            \
+      const int k = w + 4 * i;                                                                 \
+      __builtin_amdgcn_global_load_lds((const void*)(pb0 + (k0_ + k) * ldb),                   \
+                                       (lds_void*)&d_.b[k][0], 16, 0, 0);                      \
+    }                                                                                          \
   }
   d4 acc[4][4];
 #pragma unroll
@@ -184,35 +194,29 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
   const int nch = (s1 - s0) * (TB / KQ);
-  G2D_FETCH(0);
+  G2D_ISSUE(0);
   for (int c = 0; c < nch; ++c) {
-    TaskChunk& st = sm.buf[c & 1];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      st.a[ak + 2 * i][t >> 1] = ra[i].x;
-      st.a[ak + 2 * i + 1][t >> 1] = ra[i].y;
-      *reinterpret_cast<v2d*>(&st.b[bk][(t & 7) * 16 + 2 * i]) = rb[i];
+    if (c + 1 < nch) {
+      G2D_ISSUE(c + 1);
+      __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16): chunk c has landed
+    } else {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
-    __syncthreads();
+    // a bare barrier: the wait above already covers this wave's part of
+    // chunk c, and a fenced barrier would also wait for chunk c+1
+    asm volatile("s_barrier" ::: "memory");
+    const TaskChunk& st = sm.buf[c & 1];
     // every wave multiplies (a quadrant outside the target works on the
     // clamped copies and is not stored): keeping this unconditional lets the
-    // accumulators stay in the MFMA registers across chunks. The next
-    // chunk's loads are spread over the k-steps, two per step: issued in one
-    // burst they hold up the MFMA issue
-    const bool more = c + 1 < nch;
-    const int64_t k1 = (int64_t)(c + 1) * KQ;
-    const int rb0 = TB * qr + (l & 15), cb0 = TB * qc + (l & 15);
+    // accumulators stay in the MFMA registers across chunks
+    const int r0 = l & 15, cb0 = TB * qc + (l & 15);
 #pragma unroll
     for (int kk = 0; kk < KQ / 4; ++kk) {
-      if (more) {
-        ra[kk] = *reinterpret_cast<const v2d*>(pa + k1 + 2 * kk);
-        rb[kk] = *reinterpret_cast<const v2d*>(pb + k1 * ldb + 2 * kk);
-      }
-      const int k = 4 * kk + (l >> 4);
+      const int k = 4 * kk + (l >> 4), kp = 2 * kk + (l >> 5), e = (l >> 4) & 1;
       double av[4], bv[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        av[i] = st.a[k][rb0 + 16 * i];
+        av[i] = st.a[kp][TB * qr + 16 * i + r0][e];
         bv[i] = st.b[k][cb0 + 16 * i];
       }
 #pragma unroll
@@ -220,9 +224,12 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[i], bv[j], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
     }
+    // buffer c & 1 is refilled by the next iteration: every wave's reads of
+    // it are complete before the barrier, while chunk c+1 stays in flight
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   }
+#undef G2D_ISSUE
   if (active) {
     double* o = out + (int64_t)(TB * qr) * a.np + TB * qc + (int64_t)(l >> 4) * a.np + (l & 15);
     if (!ow) {  // every old value is requested before the first is used
@@ -247,7 +254,6 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * a.np + 16 * j] = acc[i][j][r];
   }
-#undef G2D_FETCH
 }
 
 // acc += A (16 x K) B (K x 16) on MFMA, both operands row-major in LDS with
@@ -653,7 +659,13 @@ Workspace workspace_carve(const Factors& f, void* base) {
 // (source row 2a-1 of tile (2a, c) and 2a of tile (2a+1, c) are the sweeping
 // workgroup's own neighbour products). The right direction is the same with
 // rows and columns exchanged. Every target gets each source once, at most one
-// delivery per launch, the first one overwriting.
+// delivery per launch, the first one (in launch order) overwriting.
+//
+// The far batches have a window of launches; they are placed earliest-
+// deadline-first into the room that each launch leaves beside its tile
+// sweeps (a launch lasts at least one tile sweep, so deliveries that fit in
+// that time on the idle compute units are free), and otherwise at their
+// deadline. Batches of one super-tile and direction get distinct launches.
 // Task word: x = dir | overwrite << 1 | (rows - 1) << 2 | (cols - 1) << 3
 // (rows, cols in tiles), y = first target tile row, z = first target tile
 // column, w = first source | (one past the last source) << 16.
@@ -661,56 +673,90 @@ void schedule_tasks(int MT, int NTt, int g, std::vector<int4>& all, std::vector<
   const int S = MT + NTt - 1;
   if (g < 1) g = 1;
   std::vector<std::vector<int4>> per(S);
-  auto emit = [&](int launch, int dir, int ow, int ti, int tj, int nr, int nc, int s0, int s1) {
-    per[launch].push_back(make_int4(dir | (ow << 1) | ((nr - 1) << 2) | ((nc - 1) << 3), ti, tj,
-                                    s0 | (s1 << 16)));
+  std::vector<double> load(S, 0.0);
+  auto work = [](int nr, int nc, int k) { return (double)nr * nc * k; };  // in 64^3 units
+  auto emit = [&](int launch, int dir, int ti, int tj, int nr, int nc, int s0, int s1) {
+    per[launch].push_back(make_int4(dir | ((nr - 1) << 2) | ((nc - 1) << 3), ti, tj, s0 | (s1 << 16)));
+    load[launch] += work(nr, nc, s1 - s0);
   };
+  struct Batch {
+    int release, deadline, slot, dir, r0, c0, nr, nc, s0, s1;
+  };
+  std::vector<Batch> batches;
+  int nslot = 0;
   for (int a = 0; 2 * a < MT; ++a) {
     for (int b = 0; 2 * b < NTt; ++b) {
       const int r0 = 2 * a, c0 = 2 * b;
       const int nr = std::min(2, MT - r0), nc = std::min(2, NTt - c0);
-      for (int dir = 0; dir < 2; ++dir) {
+      for (int dir = 0; dir < 2; ++dir, ++nslot) {
         // along: the target index that sources run along (rows for down)
         const int t0 = dir == 0 ? r0 : c0, nt = dir == 0 ? nr : nc;
         const int o0 = dir == 0 ? c0 : r0, no = dir == 0 ? nc : nr;  // the other index
-        bool first = true;
-        // far sources 0 .. t0-4, batched: each batch in a launch after its
-        // sources are swept (spread by the super-tile index), then pulled
-        // earlier where needed so that no two batches share a launch
+        // far sources 0 .. t0-4, batched; batch beta of nb may go no later
+        // than latest - (nb - 1 - beta), which keeps distinct launches
+        // feasible (its sources are swept one launch after the previous
+        // batch's at the latest)
         const int far = t0 - 4;
         const int latest = r0 + c0 - 2;  // two launches before the first sweep
-        std::vector<int> bl;
-        for (int beta = 0; beta * g <= far; ++beta) {
-          const int sl = std::min(far, beta * g + g - 1);
-          bl.push_back(std::min(latest, sl + o0 + no + (a + b) % g));
-        }
-        for (int i = (int)bl.size() - 2; i >= 0; --i) bl[i] = std::min(bl[i], bl[i + 1] - 1);
-        for (int beta = 0; beta < (int)bl.size(); ++beta) {
+        const int nbatch = far >= 0 ? far / g + 1 : 0;
+        for (int beta = 0; beta < nbatch; ++beta) {
           const int s0 = beta * g, sl = std::min(far, s0 + g - 1);
-          emit(bl[beta], dir, first, r0, c0, nr, nc, s0, sl + 1);
-          first = false;
+          batches.push_back(Batch{sl + o0 + no, latest - (nbatch - 1 - beta), nslot, dir, r0, c0, nr, nc, s0,
+                                  sl + 1});
         }
         // near sources t0-3 .. t0-2 onto both targets along, one other index at a time
         if (t0 - 2 >= 0) {
           const int s0 = std::max(0, t0 - 3);
           for (int o = o0; o < o0 + no; ++o) {
             const int launch = t0 + o - 1;
-            if (dir == 0) emit(launch, 0, first, r0, o, nt, 1, s0, t0 - 1);
-            else emit(launch, 1, first, o, c0, 1, nt, s0, t0 - 1);
+            if (dir == 0) emit(launch, 0, r0, o, nt, 1, s0, t0 - 1);
+            else emit(launch, 1, o, c0, 1, nt, s0, t0 - 1);
           }
-          first = false;
         }
         // source t0-1 onto the second target along only
         if (nt == 2 && t0 - 1 >= 0) {
           for (int o = o0; o < o0 + no; ++o) {
             const int launch = t0 + o;
-            if (dir == 0) emit(launch, 0, first, r0 + 1, o, 1, 1, t0 - 1, t0);
-            else emit(launch, 1, first, o, c0 + 1, 1, 1, t0 - 1, t0);
+            if (dir == 0) emit(launch, 0, r0 + 1, o, 1, 1, t0 - 1, t0);
+            else emit(launch, 1, o, c0 + 1, 1, 1, t0 - 1, t0);
           }
         }
       }
     }
   }
+  // room per launch beside its sweeps: the idle compute units for the
+  // duration of one tile sweep, in 64^3-product units (about 16 per unit
+  // and sweep on a 256-unit device; only the ratio between launches and the
+  // total matter for the placement)
+  std::vector<std::vector<int>> released(S);
+  for (int i = 0; i < (int)batches.size(); ++i) released[batches[i].release].push_back(i);
+  auto later = [&](int x, int y) {
+    return batches[x].deadline != batches[y].deadline ? batches[x].deadline > batches[y].deadline : x > y;
+  };
+  std::priority_queue<int, std::vector<int>, decltype(later)> avail(later);
+  std::vector<int> slot_at(nslot, -1);
+  for (int k = 0; k < S; ++k) {
+    for (int i : released[k]) avail.push(i);
+    const int nsweep = std::min(k, MT - 1) - std::max(0, k - NTt + 1) + 1;
+    const double room = 16.0 * std::max(0, 256 - nsweep);
+    std::vector<int> held;
+    while (!avail.empty()) {
+      const int i = avail.top();
+      const Batch& bt = batches[i];
+      const bool due = bt.deadline <= k;
+      if (!due && load[k] >= room) break;
+      avail.pop();
+      if (slot_at[bt.slot] == k) {  // this super-tile already has a delivery here
+        held.push_back(i);
+        continue;
+      }
+      slot_at[bt.slot] = k;
+      emit(k, bt.dir, bt.r0, bt.c0, bt.nr, bt.nc, bt.s0, bt.s1);
+    }
+    for (int i : held) avail.push(i);
+  }
+  // overwrite flag: the first delivery in launch order into each target
+  std::vector<char> seen((size_t)2 * MT * NTt, 0);
   all.clear();
   off.assign(S + 1, 0);
   for (int k = 0; k < S; ++k) {
@@ -720,6 +766,14 @@ void schedule_tasks(int MT, int NTt, int g, std::vector<int4>& all, std::vector<
       const int wy = ((y.w >> 16) - (y.w & 0xffff)) * (((y.x >> 2) & 1) + 1) * (((y.x >> 3) & 1) + 1);
       return wx > wy;
     });
+    for (int4& tk : per[k]) {
+      const int dir = tk.x & 1;
+      char& f = seen[2 * ((size_t)tk.y * NTt + tk.z) + dir];
+      if (!f) tk.x |= 2;
+      const int nr = ((tk.x >> 2) & 1) + 1, nc = ((tk.x >> 3) & 1) + 1;
+      for (int r = 0; r < nr; ++r)
+        for (int c = 0; c < nc; ++c) seen[2 * ((size_t)(tk.y + r) * NTt + tk.z + c) + dir] = 1;
+    }
     off[k] = (int)all.size();
     all.insert(all.end(), per[k].begin(), per[k].end());
   }
