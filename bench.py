@@ -36,6 +36,56 @@ WORKLOADS = {
 }
 
 
+# sources of the stage kernel: the HBM traffic taken from rocprofv3 counters
+# is reported only while these are unchanged since the counters were read
+STAGE_SOURCES = ("paper_2607_27042_amd/csrc/sweep.hip", "paper_2607_27042_amd/csrc/device.hpp",
+                 "paper_2607_27042_amd/csrc/internal.hpp", "paper_2607_27042_amd/build.py")
+
+
+def stage_sources_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in STAGE_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def stage_traffic(config: int, dtype: str):
+    """HBM bytes per stage launch from the committed counter summary of this
+    workload (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when there is
+    none or the stage kernel changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_k_stage_c{config}_{dtype}.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].split(": ", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    if fields.get("sources_sha256") != stage_sources_digest():
+        return None
+    try:
+        return float(fields["bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib: int):
+    """A plain device copy of mib MiB, three times: under rocprofv3 --pmc its
+    FETCH_SIZE / WRITE_SIZE per dispatch calibrate the counters against known
+    bytes."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -93,6 +143,8 @@ def main():
     ap.add_argument("--dtype", default=None)
     ap.add_argument("--cpu-sample", type=int, default=1536)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="run a plain MIB-MiB device copy first (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -110,6 +162,10 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+
+    if args.copy_calibration > 0:
+        log(f"copy calibration: {args.copy_calibration} MiB x 3")
+        copy_calibration(args.copy_calibration)
 
     log(f"generating config {args.config}")
     prob = wl.make_config(args.config, args.dtype)
@@ -135,31 +191,49 @@ def main():
     binding.gptq2d_round_check(f.handle, ws, stream)
     torch.cuda.synchronize()
 
+    def timed(instrument: bool):
+        """K steps bracketed by a device synchronize on both sides; with
+        instrument, every stage-kernel dispatch is also timed by HIP events
+        that take the dispatch's own start / end stamps on the round's stream
+        (this costs a few microseconds per dispatch, so the headline steps run
+        without it)."""
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        binding.gptq2d_stage_timing(f.handle, instrument)
+        start.record(stream)
+        for k in range(args.steps):
+            ev[k][0].record(stream)
+            binding.gptq2d_factor_compute(f.handle, A, B, stream)
+            ev[k][1].record(stream)
+            binding.gptq2d_round(f.handle, X, Z, Y, obj, ws, stream)
+            ev[k][2].record(stream)
+        end.record(stream)
+        torch.cuda.synchronize()
+        res = {
+            "ms_step": start.elapsed_time(end) / args.steps,
+            "t_fac": sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps,
+            "t_round": sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps,
+        }
+        binding.gptq2d_round_check(f.handle, ws, stream)
+        res["stage_total_ms"], res["stage_launches"] = binding.gptq2d_stage_time(f.handle)
+        binding.gptq2d_stage_timing(f.handle, False)
+        return res
+
     log(f"timing {args.steps} steps")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for k in range(args.steps):
-        ev[k][0].record(stream)
-        binding.gptq2d_factor_compute(f.handle, A, B, stream)
-        ev[k][1].record(stream)
-        binding.gptq2d_round(f.handle, X, Z, Y, obj, ws, stream)
-        ev[k][2].record(stream)
-    end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    ms_step = total_ms / args.steps
-    t_fac = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
-    t_round = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
-    binding.gptq2d_round_check(f.handle, ws, stream)
+    main_run = timed(False)
+    log(f"timing {args.steps} steps with per-dispatch stage events")
+    inst_run = timed(True)
+    ms_step, t_fac, t_round = main_run["ms_step"], main_run["t_fac"], main_run["t_round"]
+    stage_total_ms, stage_launches = inst_run["stage_total_ms"], inst_run["stage_launches"]
 
     stages = (m + 63) // 64 + (n + 63) // 64 - 1
     sweep_flop = m * n * (m + n)                      # m+n flop per rounded entry
     factor_flop = (5.0 / 3.0) * (m ** 3 + n ** 3)
     per_launch = sweep_flop / stages
-    stage_ms = t_round / stages                       # average stage-kernel launch (gaps included)
+    assert stage_launches == stages * args.steps, (stage_launches, stages, args.steps)
+    stage_ms = stage_total_ms / stage_launches        # average stage-kernel launch (HIP events)
     achieved = per_launch / (stage_ms * 1e-3) / 1e12
     fac_tf = factor_flop / (t_fac * 1e-3) / 1e12
     value = m * n / (ms_step * 1e-3)
@@ -181,10 +255,13 @@ def main():
                    "io_dtype": prob.dtype},
         "roofline": {
             "bound": "mfma", "achieved": achieved, "peak": PEAK_F64_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_F64_TFLOPS, "traffic": None,
+            "frac": achieved / PEAK_F64_TFLOPS, "traffic": stage_traffic(args.config, prob.dtype),
             "kernel": "k_stage (sweep stage: in-tile rounding + deferred-feedback GEMM tasks)",
             "flop_per_launch": per_launch, "launches_per_step": stages,
             "avg_launch_ms": stage_ms,
+            "launch_timing": (f"HIP events on the dispatches of {stage_launches} stage launches "
+                              f"({args.steps} further steps, round {inst_run['t_round']:.3f} ms "
+                              f"with the events)"),
         },
         "phases_ms": {"factor": t_fac, "round": t_round},
         "round_entries_per_s": m * n / (t_round * 1e-3),

@@ -150,6 +150,21 @@ const char* gptq2d_last_error(void);
 /* Library version as 10000*major + 100*minor + patch. */
 int gptq2d_version(void);
 
+/* Launch timing of the sweep's stage kernel. With enable != 0, every later
+ * gptq2d_round on f times each stage-kernel launch on the round's stream with
+ * two HIP events that take the dispatch's own start and end time stamps (the
+ * library creates them on first use and keeps them until
+ * gptq2d_factors_destroy); enable = 0 stops recording.
+ * Either call discards the pairs not yet read. Not for concurrent rounds on
+ * one handle. Errors: INVALID_ARG. */
+gptq2d_status gptq2d_stage_timing(gptq2d_factors_t f, int enable);
+
+/* Waits for the last recorded pair and returns, over all launches bracketed
+ * since the last read, the summed launch time in milliseconds (*total_ms) and
+ * the number of launches (*launches); either pointer may be NULL. Resets the
+ * record. Errors: INVALID_ARG, HIP. */
+gptq2d_status gptq2d_stage_time(gptq2d_factors_t f, double* total_ms, int64_t* launches);
+
 /* Host-only view of the deferred-feedback delivery plan of the sweep (the
  * lazy block update of Sec. 4.3 on 64 x 64 tiles), for inspection and tests;
  * touches no device. Tiles: MT = ceil(m/64) rows, NT = ceil(n/64) columns;

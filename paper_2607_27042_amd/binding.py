@@ -67,6 +67,8 @@ def load():
         "gptq2d_last_error": (ctypes.c_char_p, []),
         "gptq2d_version": (i32, []),
         "gptq2d_schedule_tasks": (i64, [i32, i32, i32, ip32, i64, ip32]),
+        "gptq2d_stage_timing": (i32, [vp, i32]),
+        "gptq2d_stage_time": (i32, [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(lib, name)
@@ -221,6 +223,18 @@ def gptq2d_round(h: int, X: torch.Tensor, Z: torch.Tensor, Y, objective, workspa
 def gptq2d_round_check(h: int, workspace: torch.Tensor, stream=None) -> None:
     _check(load().gptq2d_round_check(ctypes.c_void_p(h), _ptr(workspace), _stream(stream)),
            "gptq2d_round_check")
+
+
+def gptq2d_stage_timing(h: int, enable: bool) -> None:
+    _check(load().gptq2d_stage_timing(ctypes.c_void_p(h), int(bool(enable))), "gptq2d_stage_timing")
+
+
+def gptq2d_stage_time(h: int):
+    """(summed stage-kernel launch time in ms, launches) since the last read."""
+    ms, cnt = ctypes.c_double(0.0), ctypes.c_int64(0)
+    _check(load().gptq2d_stage_time(ctypes.c_void_p(h), ctypes.byref(ms), ctypes.byref(cnt)),
+           "gptq2d_stage_time")
+    return float(ms.value), int(cnt.value)
 
 
 def gptq2d_schedule_tasks(m: int, n: int, g: int):

@@ -35,6 +35,8 @@ static void free_all(Factors* f) {
   f->allocations.clear();
   if (f->ev_near) (void)hipEventDestroy(f->ev_near);
   if (f->ev_far) (void)hipEventDestroy(f->ev_far);
+  for (hipEvent_t ev : f->stage_ev) (void)hipEventDestroy(ev);
+  f->stage_ev.clear();
   if (f->aux) (void)hipStreamDestroy(f->aux);
   f->ev_near = f->ev_far = nullptr;
   f->aux = nullptr;
@@ -233,6 +235,33 @@ gptq2d_status gptq2d_round_check(gptq2d_factors_t f, const void* workspace, void
   if (flags & FLAG_NONFINITE) return fail(GPTQ2D_ERR_NONFINITE, "X held a NaN or an infinity");
   if (flags & FLAG_OVERFLOW) return fail(GPTQ2D_ERR_OVERFLOW, "a rounded value does not fit in int32");
   if (flags & FLAG_TIMEOUT) return fail(GPTQ2D_ERR_TIMEOUT, "a wave waited too long for its neighbour");
+  return GPTQ2D_OK;
+}
+
+gptq2d_status gptq2d_stage_timing(gptq2d_factors_t f, int enable) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  f->stage_timing = enable != 0;
+  f->stage_ev_used = 0;
+  return GPTQ2D_OK;
+}
+
+gptq2d_status gptq2d_stage_time(gptq2d_factors_t f, double* total_ms, int64_t* launches) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  double sum = 0.0;
+  const size_t used = f->stage_ev_used;
+  if (used) {
+    hipError_t e = hipEventSynchronize(f->stage_ev[used - 1]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  }
+  for (size_t i = 0; i + 1 < used; i += 2) {
+    float ms = 0.0f;
+    hipError_t e = hipEventElapsedTime(&ms, f->stage_ev[i], f->stage_ev[i + 1]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    sum += ms;
+  }
+  if (total_ms) *total_ms = sum;
+  if (launches) *launches = (int64_t)(used / 2);
+  f->stage_ev_used = 0;
   return GPTQ2D_OK;
 }
 

@@ -44,6 +44,12 @@ struct Factors {
   hipStream_t aux = nullptr;
   hipEvent_t ev_near = nullptr, ev_far = nullptr;
   Schedule sched;
+  // launch timing of the sweep's stage kernel (diagnostics): while enabled,
+  // every stage launch records its start and end time stamps into a pair of
+  // events; the pairs accumulate until they are read
+  bool stage_timing = false;
+  mutable std::vector<hipEvent_t> stage_ev;  // event pool, grows on demand
+  mutable size_t stage_ev_used = 0;          // events recorded since the last read
   std::vector<void*> allocations;
 };
 

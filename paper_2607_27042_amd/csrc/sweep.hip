@@ -21,6 +21,7 @@
 // anti-diagonals (rank up to 64 g), never later than the launch before the
 // target is swept. Each (target, direction) gets at most one task per launch,
 // so accumulation needs no atomics and the result is deterministic.
+#include <hip/hip_ext.h>
 #include <math.h>
 
 #include <algorithm>
@@ -80,13 +81,15 @@ struct SweepSmem {
 
 // Staging of one 32-deep chunk of a delivery product, filled by direct
 // global -> LDS loads (each wave instruction moves 64 lanes x 16 bytes to 1 KB
-// of consecutive LDS): the left operand as a[kp][row][e] = A[row][2 kp + e]
-// (128 rows, so each 1 KB block holds one k-pair of 64 rows), the right
-// operand as rows b[k][col] padded to 130 doubles. Both layouts make an MFMA
-// operand read take the minimum two LDS passes.
+// of consecutive LDS): the left operand in blocks of four rows, each row's
+// 16-byte pieces permuted by an XOR with the row's position in the block and
+// every block padded by 64 bytes (an MFMA operand read of 16 rows then hits 16
+// distinct bank groups), the right operand as rows b[k][col] padded to 130
+// doubles. Every load instruction reads whole 256-byte row segments.
 constexpr int KQ = 32;
+constexpr int AQ = 4 * KQ + 8;  // doubles per 4-row block of the left operand (64 B pad)
 struct TaskChunk {
-  double a[KQ / 2][2 * TB][2];
+  double a[2 * TB / 4][AQ];
   double b[KQ][2 * TB + 2];
 };
 struct TaskSmem {
@@ -169,20 +172,24 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
   const int qr = w >> 1, qc = w & 1;
   const bool active = qr < nr && qc < nc;
   typedef __attribute__((address_space(3))) void lds_void;
-  // this lane's source rows / columns (clamped to the target)
-  const double* pa0 = Ap + (int64_t)min(l, TB * nr - 1) * lda;          // A row l (first half)
-  const double* pa1 = Ap + (int64_t)min(TB + l, TB * nr - 1) * lda;     // A row 64 + l
+  // this lane's source rows / columns (clamped to the target). Left operand: instruction j moves rows 4j .. 4j+3 of the chunk, lane l
+  // the 16-byte piece (l & 15) ^ r of row 4j + r (r = l >> 4), so that the
+  // 16 rows an MFMA operand read touches fall in distinct LDS banks
+  const int ar = l >> 4, ap = (l & 15) ^ ar;
+  const double* pa[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    pa[i] = Ap + (int64_t)min(4 * (w + 4 * i) + ar, TB * nr - 1) * lda + 2 * ap;
   const double* pb0 = Bp + min(2 * l, TB * nc - 2);                      // B columns 2l, 2l+1
-  // wave w moves A blocks j = w + 4i (k-pair j >> 1, row half j & 1) and B
-  // rows k = w + 4i, i = 0..7
+  // wave w moves the A row blocks j = w + 4i and the B rows k = w + 4i,
+  // i = 0..7
 #define G2D_ISSUE(C_)                                                                          \
   {                                                                                            \
     TaskChunk& d_ = sm.buf[(C_) & 1];                                                          \
     const int64_t k0_ = (int64_t)(C_) * KQ;                                                    \
     _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                            \
-      const int j = w + 4 * i, kp = j >> 1, hf = j & 1;                                        \
-      __builtin_amdgcn_global_load_lds((const void*)((hf ? pa1 : pa0) + k0_ + 2 * kp),         \
-                                       (lds_void*)&d_.a[kp][TB * hf][0], 16, 0, 0);            \
+      __builtin_amdgcn_global_load_lds((const void*)(pa[i] + k0_),                             \
+                                       (lds_void*)&d_.a[w + 4 * i][0], 16, 0, 0);              \
       const int k = w + 4 * i;                                                                 \
       __builtin_amdgcn_global_load_lds((const void*)(pb0 + (k0_ + k) * ldb),                   \
                                        (lds_void*)&d_.b[k][0], 16, 0, 0);                      \
@@ -213,10 +220,11 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
 #pragma unroll
     for (int kk = 0; kk < KQ / 4; ++kk) {
       const int k = 4 * kk + (l >> 4), kp = 2 * kk + (l >> 5), e = (l >> 4) & 1;
+      const int rr = r0 & 3, ao = KQ * rr + 2 * (kp ^ rr) + e;
       double av[4], bv[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        av[i] = st.a[kp][TB * qr + 16 * i + r0][e];
+        av[i] = st.a[(TB * qr + 16 * i + r0) >> 2][ao];
         bv[i] = st.b[k][cb0 + 16 * i];
       }
 #pragma unroll
@@ -840,7 +848,21 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
     a.nsweep = ihi - ilo + 1;
     const int ntasks = S.offset[k + 1] - S.offset[k];
     a.tasks = S.d_tasks ? S.d_tasks + S.offset[k] : nullptr;
-    hipLaunchKernelGGL(k_stage<T>, dim3(a.nsweep + ntasks), dim3(NT), 0, s, a);
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (f.stage_timing) {
+      while (f.stage_ev.size() < f.stage_ev_used + 2) {
+        hipEvent_t ev;
+        hipError_t e = hipEventCreate(&ev);
+        if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+        f.stage_ev.push_back(ev);
+      }
+      e0 = f.stage_ev[f.stage_ev_used];
+      e1 = f.stage_ev[f.stage_ev_used + 1];
+      f.stage_ev_used += 2;
+    }
+    // with timing on, the two events take the start and end time stamps of
+    // the dispatch itself (no marker packets between the launches)
+    hipExtLaunchKernelGGL(k_stage<T>, dim3(a.nsweep + ntasks), dim3(NT), 0, s, e0, e1, 0, a);
   }
   if (objective)
     hipLaunchKernelGGL(k_obj_reduce, dim3(1), dim3(NT), 0, s, ws.objp, f.MT * f.NT, objective);

@@ -148,3 +148,25 @@ def test_argument_errors():
     assert ei.value.status == -6
     with pytest.raises(ValueError):
         binding.gptq2d_round(f.handle, X[:, :40], Z, None, None, f.workspace())
+
+
+def test_stage_timing_is_transparent():
+    """Timing the stage launches with events changes no result, and the
+    record counts one pair per stage launch (MT + NT - 1 per round)."""
+    p = wl.random_problem(200, 330, 10, "f32", "wishart")
+    f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B))
+    X = pr.to_dev(p.X)
+    Z0, Y0, o0 = binding.round_matrix(f, X)
+    binding.gptq2d_stage_timing(f.handle, True)
+    Z1, Y1, o1 = binding.round_matrix(f, X)
+    Z2, Y2, o2 = binding.round_matrix(f, X)
+    ms, cnt = binding.gptq2d_stage_time(f.handle)
+    assert cnt == 2 * ((200 + 63) // 64 + (330 + 63) // 64 - 1)
+    assert ms > 0.0
+    assert binding.gptq2d_stage_time(f.handle) == (0.0, 0)
+    binding.gptq2d_stage_timing(f.handle, False)
+    binding.round_matrix(f, X)
+    assert binding.gptq2d_stage_time(f.handle)[1] == 0
+    for Z, Y, o in ((Z1, Y1, o1), (Z2, Y2, o2)):
+        assert torch.equal(Z, Z0) and torch.equal(Y, Y0) and float(o[0]) == float(o0[0])
+    f.close()
