@@ -17,7 +17,12 @@ ARCH = "gfx950"
 FLAGS = [
     "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-shared",
     # keep the compiler from emitting packed fp32 VALU instructions
-    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs (no copies between register files)
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
+    # a single lane's atomic is issued as written: no wave-wide rewrite that
+    # waits for its result (and every other outstanding load) at once
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
 ]
 

@@ -25,6 +25,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <functional>
 #include <queue>
 #include <vector>
 
@@ -51,7 +52,8 @@ struct StageArgs {
   double* C;
   double* objp;
   int* flags;
-  const int4* tasks;
+  const int4* tasks;  // this launch's deliveries, grouped by bin
+  const int2* bins;   // this launch's bins (one work group each)
   int stage, ilo, nsweep;
 };
 
@@ -113,15 +115,10 @@ __device__ __forceinline__ double load_x(const T* X, int64_t ldx, int gi, int gj
   return ok ? (double)v : 0.0;
 }
 
-// One deferred-feedback delivery (a GEMM task): out (+)= A B with A the
-// (64 nr) x K source panel and B the K x (64 nc) panel, nr, nc in {1, 2},
-// K = 64 (number of source tiles). Wave w owns the 64 x 64 output quadrant
-// (w >> 1, w & 1) as 4 x 4 MFMA blocks; quadrants outside the target are
-// skipped. 32-deep chunks go global -> registers -> LDS, double-buffered, so
-// the loads of chunk c+1 are in flight while chunk c is on MFMA; rows or
-// columns past the target are loaded from a clamped address and never used.
-// A single 64 x 64 target: the four waves split it 32 x 32 each (Acc), and
-// 64-deep blocks go global -> registers -> LDS, double-buffered.
+// A deferred-feedback delivery onto a single 64 x 64 target: out (+)= A B
+// with A the 64 x (64 nb) source panel and B the (64 nb) x 64 panel. The four
+// waves split the target 32 x 32 each (Acc); 64-deep blocks go global ->
+// registers -> LDS, double-buffered.
 __device__ void run_task64(const double* Ap, int64_t lda, const double* Bp, int64_t ldb,
                            double* out, int64_t ldo, int nb, int ow, TaskSmem& sm) {
   Acc acc;
@@ -144,79 +141,130 @@ __device__ void run_task64(const double* Ap, int64_t lda, const double* Bp, int6
   acc_store(acc, out, ldo, 1.0);
 }
 
-__device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
-  const int dir = tk.x & 1, ow = (tk.x >> 1) & 1;
-  const int nr = ((tk.x >> 2) & 1) + 1, nc = ((tk.x >> 3) & 1) + 1;
-  const int ti = tk.y, tj = tk.z, s0 = tk.w & 0xffff, s1 = tk.w >> 16;
-  const double* Ap;
-  const double* Bp;
-  int64_t lda;
+// Operands of one delivery (uniform over the work group): out (+)= A B with
+// A the (64 nr) x (64 K) source panel and B the (64 K) x (64 nc) panel.
+struct TaskOp {
+  const double* A;
+  const double* B;
   double* out;
+  int64_t lda;
+  int nch, ow, nr, nc;
+};
+
+__device__ __forceinline__ TaskOp task_op(const StageArgs& a, int4 tk) {
+  const int dir = tk.x & 1;
+  const int ti = tk.y, tj = tk.z, s0 = tk.w & 0xffff, s1 = tk.w >> 16;
+  TaskOp T;
+  T.ow = (tk.x >> 1) & 1;
+  T.nr = ((tk.x >> 2) & 1) + 1;
+  T.nc = ((tk.x >> 3) & 1) + 1;
+  T.nch = (s1 - s0) * (TB / KQ);
   if (dir == 0) {
-    Ap = a.L + (int64_t)ti * TB * a.mp + (int64_t)s0 * TB;
-    lda = a.mp;
-    Bp = a.E + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
-    out = a.P + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
+    T.A = a.L + (int64_t)ti * TB * a.mp + (int64_t)s0 * TB;
+    T.lda = a.mp;
+    T.B = a.E + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
+    T.out = a.P + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
   } else {
-    Ap = a.C + (int64_t)ti * TB * a.np + (int64_t)s0 * TB;
-    lda = a.np;
-    Bp = a.U + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
-    out = a.R + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
+    T.A = a.C + (int64_t)ti * TB * a.np + (int64_t)s0 * TB;
+    T.lda = a.np;
+    T.B = a.U + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
+    T.out = a.R + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
   }
-  const int64_t ldb = a.np;
-  if (nr == 1 && nc == 1) {
-    run_task64(Ap, lda, Bp, ldb, out, a.np, s1 - s0, ow, sm);
-    return;
+  return T;
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Chunk c of task T into d: wave w moves the left-operand row blocks
+// j = w + 4i (rows 4j .. 4j+3) and the right-operand rows k = w + 4i,
+// i = 0..7, sixteen 1 KB direct global -> LDS loads in all. Lane l of a
+// left-operand load takes the 16-byte piece (l & 15) ^ (l >> 4) of row
+// 4j + (l >> 4); rows and columns past the target are read from a clamped
+// address (never used).
+__device__ __forceinline__ void task_issue(const TaskOp& T, int c, TaskChunk& d, int w, int l,
+                                           int64_t ldb) {
+  const int ar = l >> 4, ap = (l & 15) ^ ar;
+  const int64_t k0 = (int64_t)c * KQ;
+  const double* pb = T.B + min(2 * l, TB * T.nc - 2) + k0 * ldb;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int j = w + 4 * i;
+    const double* pa = T.A + (int64_t)min(4 * j + ar, TB * T.nr - 1) * T.lda + 2 * ap + k0;
+    __builtin_amdgcn_global_load_lds((const void*)pa, (lds_void*)&d.a[j][0], 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(pb + j * ldb), (lds_void*)&d.b[j][0], 16, 0, 0);
   }
+}
+
+// Accumulator of wave (qr, qc): the old target values (a delivery that adds)
+// or zero (one that overwrites, or a quadrant outside the target).
+__device__ __forceinline__ void task_init(d4 (&acc)[4][4], const TaskOp& T, int qr, int qc, int l,
+                                          int64_t np) {
+  if (qr < T.nr && qc < T.nc && !T.ow) {
+    const double* o = T.out + (int64_t)(TB * qr) * np + TB * qc + (int64_t)(l >> 4) * np + (l & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[i][j][r] = o[(int64_t)(16 * i + 4 * r) * np + 16 * j];
+    // the accumulators are complete before the chunk loop (so that no wait
+    // for them lands inside it, where it would also wait for the next chunk)
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
+  }
+}
+
+__device__ __forceinline__ void task_store(const d4 (&acc)[4][4], const TaskOp& T, int qr, int qc,
+                                           int l, int64_t np) {
+  if (qr < T.nr && qc < T.nc) {
+    double* o = T.out + (int64_t)(TB * qr) * np + TB * qc + (int64_t)(l >> 4) * np + (l & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * np + 16 * j] = acc[i][j][r];
+  }
+}
+
+// A run of deliveries with a 128-wide target (nr or nc = 2), streamed
+// through one double-buffered pipeline: the first chunk of the next task is
+// loaded while the last chunk of the current one is on MFMA, so tasks follow
+// each other without a pipeline drain. Wave w owns the 64 x 64 output
+// quadrant (w >> 1, w & 1) as 4 x 4 MFMA blocks; every wave multiplies (a
+// quadrant outside the target works on the clamped copies and is not
+// stored), which keeps the accumulators in the MFMA registers.
+__device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& sm) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   const int qr = w >> 1, qc = w & 1;
-  const bool active = qr < nr && qc < nc;
-  typedef __attribute__((address_space(3))) void lds_void;
-  // this lane's source rows / columns (clamped to the target). Left operand: instruction j moves rows 4j .. 4j+3 of the chunk, lane l
-  // the 16-byte piece (l & 15) ^ r of row 4j + r (r = l >> 4), so that the
-  // 16 rows an MFMA operand read touches fall in distinct LDS banks
-  const int ar = l >> 4, ap = (l & 15) ^ ar;
-  const double* pa[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-    pa[i] = Ap + (int64_t)min(4 * (w + 4 * i) + ar, TB * nr - 1) * lda + 2 * ap;
-  const double* pb0 = Bp + min(2 * l, TB * nc - 2);                      // B columns 2l, 2l+1
-  // wave w moves the A row blocks j = w + 4i and the B rows k = w + 4i,
-  // i = 0..7
-#define G2D_ISSUE(C_)                                                                          \
-  {                                                                                            \
-    TaskChunk& d_ = sm.buf[(C_) & 1];                                                          \
-    const int64_t k0_ = (int64_t)(C_) * KQ;                                                    \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                            \
-      __builtin_amdgcn_global_load_lds((const void*)(pa[i] + k0_),                             \
-                                       (lds_void*)&d_.a[w + 4 * i][0], 16, 0, 0);              \
-      const int k = w + 4 * i;                                                                 \
-      __builtin_amdgcn_global_load_lds((const void*)(pb0 + (k0_ + k) * ldb),                   \
-                                       (lds_void*)&d_.b[k][0], 16, 0, 0);                      \
-    }                                                                                          \
-  }
+  const int64_t np = a.np;
+  const int r0 = l & 15, cb0 = TB * qc + (l & 15);
   d4 acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
-  const int nch = (s1 - s0) * (TB / KQ);
-  G2D_ISSUE(0);
-  for (int c = 0; c < nch; ++c) {
-    if (c + 1 < nch) {
-      G2D_ISSUE(c + 1);
+  TaskOp T = task_op(a, tk[0]);
+  TaskOp Tn = T;
+  task_issue(T, 0, sm.buf[0], w, l, np);
+  task_init(acc, T, qr, qc, l, np);
+  int idx = 0, c = 0, p = 0;
+  for (;;) {
+    const bool last = c + 1 == T.nch;
+    if (!last) {
+      task_issue(T, c + 1, sm.buf[p ^ 1], w, l, np);
       __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16): chunk c has landed
+    } else if (idx + 1 < n) {
+      Tn = task_op(a, tk[idx + 1]);
+      task_issue(Tn, 0, sm.buf[p ^ 1], w, l, np);
+      __builtin_amdgcn_s_waitcnt(0x4f70);
     } else {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
     // a bare barrier: the wait above already covers this wave's part of
-    // chunk c, and a fenced barrier would also wait for chunk c+1
+    // chunk c, and a fenced barrier would also wait for the next chunk
     asm volatile("s_barrier" ::: "memory");
-    const TaskChunk& st = sm.buf[c & 1];
-    // every wave multiplies (a quadrant outside the target works on the
-    // clamped copies and is not stored): keeping this unconditional lets the
-    // accumulators stay in the MFMA registers across chunks
-    const int r0 = l & 15, cb0 = TB * qc + (l & 15);
+    const TaskChunk& st = sm.buf[p];
 #pragma unroll
     for (int kk = 0; kk < KQ / 4; ++kk) {
       const int k = 4 * kk + (l >> 4), kp = 2 * kk + (l >> 5), e = (l >> 4) & 1;
@@ -233,34 +281,33 @@ __device__ void run_task(const StageArgs& a, int4 tk, TaskSmem& sm) {
         for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[i], bv[j], acc[i][j], 0, 0, 0);
     }
-    // buffer c & 1 is refilled by the next iteration: every wave's reads of
-    // it are complete before the barrier, while chunk c+1 stays in flight
+    // buffer p is refilled next: every wave's reads of it are complete
+    // before the barrier, while the next chunk stays in flight
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  }
-#undef G2D_ISSUE
-  if (active) {
-    double* o = out + (int64_t)(TB * qr) * a.np + TB * qc + (int64_t)(l >> 4) * a.np + (l & 15);
-    if (!ow) {  // every old value is requested before the first is used
-      double old[4][4][4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) old[i][j][r] = o[(int64_t)(16 * i + 4 * r) * a.np + 16 * j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[i][j][r] += old[i][j][r];
+    p ^= 1;
+    if (last) {
+      task_store(acc, T, qr, qc, l, np);
+      if (++idx == n) break;
+      T = Tn;
+      c = 0;
+      task_init(acc, T, qr, qc, l, np);
+    } else {
+      ++c;
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * a.np + 16 * j] = acc[i][j][r];
+  }
+}
+
+// One bin of a launch's deliveries, bin = {first task, streamed count |
+// single-tile count << 16}: the 128-wide ones first through the stream,
+// the single-tile ones after it.
+__device__ void run_bin(const StageArgs& a, int2 bin, TaskSmem& sm) {
+  const int4* tk = a.tasks + bin.x;
+  const int ns = bin.y & 0xffff, n1 = bin.y >> 16;
+  if (ns > 0) run_stream(a, tk, ns, sm);
+  for (int i = 0; i < n1; ++i) {
+    if (ns > 0 || i > 0) __syncthreads();  // the staging buffers are reused
+    const TaskOp T = task_op(a, tk[ns + i]);
+    run_task64(T.A, T.lda, T.B, a.np, T.out, a.np, T.nch / (TB / KQ), T.ow, sm);
   }
 }
 
@@ -608,7 +655,7 @@ __global__ __launch_bounds__(NT) void k_stage(StageArgs a) {
     const int I = a.ilo + b;
     run_sweep<T>(a, I, a.stage - I, sm.s);
   } else {
-    run_task(a, a.tasks[b - a.nsweep], sm.t);
+    run_bin(a, a.bins[b - a.nsweep], sm.t);
   }
 }
 
@@ -788,9 +835,72 @@ void schedule_tasks(int MT, int NTt, int g, std::vector<int4>& all, std::vector<
   off[S] = (int)all.size();
 }
 
+// Bins of a stage: one per compute unit, filled longest-processing-time
+// first with an estimated cost per task (in microseconds: about 3.6 per
+// 32-deep chunk of a 128-wide product, 5 per 64-deep block of a single-tile
+// one, plus a start cost), so that the bins finish close together; a work
+// group per non-empty bin, after the sweeps. The first units - nsweep bins
+// start beside the sweeps; the others only when a sweep is done, so they
+// start loaded with its duration (and stay empty when the work fits beside
+// the sweeps). In a bin the 128-wide tasks come first (they share one
+// streamed pipeline), the single-tile ones after them.
+constexpr double kSweepCost = 45.0;  // one tile sweep, microseconds
+void pack_bins(int MT, int NTt, int units, std::vector<int4>& all, const std::vector<int>& off,
+               std::vector<int2>& bins, std::vector<int>& boff) {
+  const int S = MT + NTt - 1;
+  bins.clear();
+  boff.assign(S + 1, 0);
+  std::vector<int4> out;
+  out.reserve(all.size());
+  auto small = [](const int4& x) { return ((x.x >> 2) & 3) == 0; };
+  auto cost = [&](const int4& x) {
+    const int K = (x.w >> 16) - (x.w & 0xffff);
+    return small(x) ? 2.0 + 5.0 * K : 1.0 + 3.6 * 2 * K;
+  };
+  for (int k = 0; k < S; ++k) {
+    boff[k] = (int)bins.size();
+    const int n = off[k + 1] - off[k];
+    if (n == 0) continue;
+    const int nsweep = std::min(k, MT - 1) - std::max(0, k - NTt + 1) + 1;
+    const int nfree = std::max(0, units - nsweep);
+    const int nb = std::max(1, units);
+    std::vector<int> order(n);
+    for (int i = 0; i < n; ++i) order[i] = off[k] + i;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int x, int y) { return cost(all[x]) > cost(all[y]); });
+    std::vector<std::vector<int>> member(nb);
+    // least-loaded bin first (ties: lowest index)
+    typedef std::pair<double, int> Load;
+    std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
+    for (int b = 0; b < nb; ++b) heap.push(Load(b < nfree ? 0.0 : kSweepCost, b));
+    for (int i : order) {
+      Load top = heap.top();
+      heap.pop();
+      member[top.second].push_back(i);
+      top.first += cost(all[i]);
+      heap.push(top);
+    }
+    const int base = (int)out.size();
+    for (int b = 0; b < nb; ++b) {
+      if (member[b].empty()) continue;
+      const int first = (int)out.size() - base;
+      int ns = 0, n1 = 0;
+      for (int i : member[b])
+        if (!small(all[i])) out.push_back(all[i]), ++ns;
+      for (int i : member[b])
+        if (small(all[i])) out.push_back(all[i]), ++n1;
+      bins.push_back(make_int2(first, ns | (n1 << 16)));
+    }
+  }
+  boff[S] = (int)bins.size();
+  all.swap(out);
+}
+
 void free_schedule(Schedule& sc) {
   if (sc.d_tasks) (void)hipFree(sc.d_tasks);
+  if (sc.d_bins) (void)hipFree(sc.d_bins);
   sc.d_tasks = nullptr;
+  sc.d_bins = nullptr;
 }
 
 gptq2d_status build_schedule(Factors& f, int g) {
@@ -798,16 +908,28 @@ gptq2d_status build_schedule(Factors& f, int g) {
   std::vector<int> off;
   if (g < 1) g = 1;
   schedule_tasks(f.MT, f.NT, g, all, off);
+  int units = 0;
+  if (hipDeviceGetAttribute(&units, hipDeviceAttributeMultiprocessorCount, f.device) != hipSuccess ||
+      units <= 0)
+    units = 256;
+  std::vector<int2> bins;
+  std::vector<int> boff;
+  pack_bins(f.MT, f.NT, units, all, off, bins, boff);
   free_schedule(f.sched);
   if (!all.empty()) {
     hipError_t e = hipMalloc(&f.sched.d_tasks, all.size() * sizeof(int4));
     if (e != hipSuccess) return hip_fail(e, "schedule allocation");
     e = hipMemcpy(f.sched.d_tasks, all.data(), all.size() * sizeof(int4), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "schedule upload");
+    e = hipMalloc(&f.sched.d_bins, bins.size() * sizeof(int2));
+    if (e != hipSuccess) return hip_fail(e, "schedule allocation");
+    e = hipMemcpy(f.sched.d_bins, bins.data(), bins.size() * sizeof(int2), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "schedule upload");
   }
   f.sched.g = g;
   f.sched.stages = f.MT + f.NT - 1;
   f.sched.offset = off;
+  f.sched.bin_offset = boff;
   f.sched.ntasks = all.size();
   return GPTQ2D_OK;
 }
@@ -846,8 +968,9 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
     a.stage = k;
     a.ilo = ilo;
     a.nsweep = ihi - ilo + 1;
-    const int ntasks = S.offset[k + 1] - S.offset[k];
+    const int ntasks = S.bin_offset[k + 1] - S.bin_offset[k];  // work groups beside the sweeps
     a.tasks = S.d_tasks ? S.d_tasks + S.offset[k] : nullptr;
+    a.bins = S.d_bins ? S.d_bins + S.bin_offset[k] : nullptr;
     hipEvent_t e0 = nullptr, e1 = nullptr;
     if (f.stage_timing) {
       while (f.stage_ev.size() < f.stage_ev_used + 2) {
