@@ -403,31 +403,42 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
   }
 
   // Algorithm 3 on the 16 x 16 sub-tile, one 2 x 2 block per lane. The
-  // blocks form an 8 x 8 grid swept along its anti-diagonals: in step k the
-  // lanes with p + q == k round their four entries (an in-block chain of
-  // three entry anti-diagonals), and every lane first adds the feedback of
-  // the blocks finished in step k-1 in its block column (errors through L,
-  // Alg. 3 push down) and block row (C through U, push right). Finished
-  // blocks publish E and C into Et / Ct, read back in the next step by the
-  // same wave (LDS is in order within a wave: no barrier).
+  // blocks form an 8 x 8 grid swept along its anti-diagonals: block (p, q)
+  // is rounded in step p + q (an in-block chain of three entry
+  // anti-diagonals). In every step each lane first adds the feedback of the
+  // blocks finished in the step before that lie above it in its block column
+  // (errors through L, Alg. 3 push down) or left of it in its block row (C
+  // through U, push right); other source positions get a zero weight (the
+  // zero column of Ls, the zero rows of Us) and a zero operand.
+  // So a lane's accumulators stop changing after its own step, and every
+  // lane runs the rounding chain in every step without a branch: before its
+  // step it publishes finite placeholders that nobody reads with a nonzero
+  // weight, from its step on the final E and C of its block (read back by
+  // the same wave in the next step: LDS is in order within a wave, no
+  // barrier). The results of the last step are every lane's final values.
   const double u01 = sm.Us[uc + 2 * q][uc + 2 * q + 1];
+  double* const eown = &sm.x.t.Et[br][uc + 2 * q];
+  double* const cown = &sm.x.t.Ct[br][uc + 2 * q];
+  const double* const zpad = &sm.Us[TB][0];  // two zero rows: the unused sources
   double yf[2][2], cf[2][2];
-#pragma unroll 1
+#pragma unroll
   for (int k = 0; k < SS - 1; ++k) {
-    const int sr = k - 1 - q, sc = k - 1 - p;  // source block row / column
-    const bool vr = sr >= 0 && sr < SS / 2, vc = sc >= 0 && sc < SS / 2;
-    const int er = SS * w + 2 * (vr ? sr : 0);  // tile row of the source errors
-    const int lc = vr ? er : TB;                 // L column (zero column if none)
-    const int cc = uc + 2 * (vc ? sc : 0);       // tile column of the source C
-    const int ur = vc ? cc : TB;                 // U row (zero row if none)
-    const double2 e0 = *reinterpret_cast<const double2*>(&sm.x.t.Et[er][uc + 2 * q]);
-    const double2 e1 = *reinterpret_cast<const double2*>(&sm.x.t.Et[er + 1][uc + 2 * q]);
-    const double2 l0 = *reinterpret_cast<const double2*>(&sm.Ls[br][lc]);
-    const double2 l1 = *reinterpret_cast<const double2*>(&sm.Ls[br + 1][lc]);
-    const double2 c0 = *reinterpret_cast<const double2*>(&sm.x.t.Ct[br][cc]);
-    const double2 c1 = *reinterpret_cast<const double2*>(&sm.x.t.Ct[br + 1][cc]);
-    const double2 v0 = *reinterpret_cast<const double2*>(&sm.Us[ur][uc + 2 * q]);
-    const double2 v1 = *reinterpret_cast<const double2*>(&sm.Us[ur + 1][uc + 2 * q]);
+    const bool vr = (unsigned)(k - 1 - q) < (unsigned)p;  // source block row k-1-q above
+    const bool vc = (unsigned)(k - 1 - p) < (unsigned)q;  // source block column k-1-p left
+    const int er = SS * w + 2 * (k - 1 - q);                // its tile row
+    const int cc = uc + 2 * (k - 1 - p);                    // its tile column
+    const double* pe = vr ? &sm.x.t.Et[0][0] + er * TP + uc + 2 * q : zpad;
+    const double* pl = &sm.Ls[br][0] + (vr ? er : TB);
+    const double* pc = vc ? &sm.x.t.Ct[0][0] + br * TP + cc : zpad;
+    const double* pu = &sm.Us[0][0] + (vc ? cc : TB) * TP + uc + 2 * q;
+    const double2 e0 = *reinterpret_cast<const double2*>(pe);
+    const double2 e1 = *reinterpret_cast<const double2*>(pe + TP);
+    const double2 l0 = *reinterpret_cast<const double2*>(pl);
+    const double2 l1 = *reinterpret_cast<const double2*>(pl + TP);
+    const double2 c0 = *reinterpret_cast<const double2*>(pc);
+    const double2 c1 = *reinterpret_cast<const double2*>(pc + TP);
+    const double2 v0 = *reinterpret_cast<const double2*>(pu);
+    const double2 v1 = *reinterpret_cast<const double2*>(pu + TP);
     Dc[0][0] = fma(l0.y, e1.x, fma(l0.x, e0.x, Dc[0][0]));
     Dc[0][1] = fma(l0.y, e1.y, fma(l0.x, e0.y, Dc[0][1]));
     Dc[1][0] = fma(l1.y, e1.x, fma(l1.x, e0.x, Dc[1][0]));
@@ -436,25 +447,25 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
     Rc[0][1] = fma(c0.y, v1.y, fma(c0.x, v0.y, Rc[0][1]));
     Rc[1][0] = fma(c1.y, v1.x, fma(c1.x, v0.x, Rc[1][0]));
     Rc[1][1] = fma(c1.y, v1.y, fma(c1.x, v0.y, Rc[1][1]));
-    if (p + q == k) {
-      const double y00 = Rc[0][0] + Dc[0][0];
-      const double e00 = rint(y00) - y00;
-      const double c00 = Dc[0][0] + e00;
-      const double d10 = fma(b.l10, e00, Dc[1][0]);
-      const double y01 = fma(c00, u01, Rc[0][1]) + Dc[0][1];
-      const double e01 = rint(y01) - y01;
-      const double c01 = Dc[0][1] + e01;
-      const double y10 = Rc[1][0] + d10;
-      const double e10 = rint(y10) - y10;
-      const double c10 = d10 + e10;
-      const double d11 = fma(b.l10, e01, Dc[1][1]);
-      const double y11 = fma(c10, u01, Rc[1][1]) + d11;
-      const double e11 = rint(y11) - y11;
-      const double c11 = d11 + e11;
-      *reinterpret_cast<double2*>(&sm.x.t.Et[br][uc + 2 * q]) = double2{e00, e01};
-      *reinterpret_cast<double2*>(&sm.x.t.Et[br + 1][uc + 2 * q]) = double2{e10, e11};
-      *reinterpret_cast<double2*>(&sm.x.t.Ct[br][uc + 2 * q]) = double2{c00, c01};
-      *reinterpret_cast<double2*>(&sm.x.t.Ct[br + 1][uc + 2 * q]) = double2{c10, c11};
+    const double y00 = Rc[0][0] + Dc[0][0];
+    const double e00 = rint(y00) - y00;
+    const double c00 = Dc[0][0] + e00;
+    const double d10 = fma(b.l10, e00, Dc[1][0]);
+    const double y01 = fma(c00, u01, Rc[0][1]) + Dc[0][1];
+    const double e01 = rint(y01) - y01;
+    const double c01 = Dc[0][1] + e01;
+    const double y10 = Rc[1][0] + d10;
+    const double e10 = rint(y10) - y10;
+    const double c10 = d10 + e10;
+    const double d11 = fma(b.l10, e01, Dc[1][1]);
+    const double y11 = fma(c10, u01, Rc[1][1]) + d11;
+    const double e11 = rint(y11) - y11;
+    const double c11 = d11 + e11;
+    *reinterpret_cast<double2*>(eown) = double2{e00, e01};
+    *reinterpret_cast<double2*>(eown + TP) = double2{e10, e11};
+    *reinterpret_cast<double2*>(cown) = double2{c00, c01};
+    *reinterpret_cast<double2*>(cown + TP) = double2{c10, c11};
+    if (k == SS - 2) {
       yf[0][0] = y00; yf[0][1] = y01; yf[1][0] = y10; yf[1][1] = y11;
       cf[0][0] = c00; cf[0][1] = c01; cf[1][0] = c10; cf[1][1] = c11;
     }
