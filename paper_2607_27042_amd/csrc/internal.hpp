@@ -22,7 +22,7 @@ struct Schedule {
   std::vector<int> offset;       // per stage: first task (size stages + 1)
   std::vector<int> bin_offset;   // per stage: first bin (size stages + 1)
   int4* d_tasks = nullptr;       // all tasks, grouped by stage, then by bin
-  int2* d_bins = nullptr;        // {first task in the stage, counts}, grouped by stage
+  int4* d_bins = nullptr;        // {first task in the stage, counts by shape}, grouped by stage
   size_t ntasks = 0;
 };
 
@@ -83,8 +83,9 @@ gptq2d_status launch_import(Factors& f, const double* L, int64_t ldl, const doub
 void schedule_tasks(int MT, int NT, int g, std::vector<int4>& all, std::vector<int>& offset);
 // Packs each stage's tasks into bins (one work group each) for `units`
 // compute units; reorders `all` within every stage.
-void pack_bins(int MT, int NT, int units, std::vector<int4>& all, const std::vector<int>& offset,
-               std::vector<int2>& bins, std::vector<int>& bin_offset);
+gptq2d_status pack_bins(int MT, int NT, int units, std::vector<int4>& all,
+                        const std::vector<int>& offset, std::vector<int4>& bins,
+                        std::vector<int>& bin_offset);
 gptq2d_status build_schedule(Factors& f, int g);
 void free_schedule(Schedule& s);
 gptq2d_status launch_round(const Factors& f, gptq2d_dtype dt, const void* X, int64_t ldx,

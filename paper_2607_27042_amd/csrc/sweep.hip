@@ -53,7 +53,7 @@ struct StageArgs {
   double* objp;
   int* flags;
   const int4* tasks;  // this launch's deliveries, grouped by bin
-  const int2* bins;   // this launch's bins (one work group each)
+  const int4* bins;   // this launch's bins (one work group each)
   int stage, ilo, nsweep;
 };
 
@@ -95,10 +95,7 @@ struct TaskChunk {
   double b[KQ][2 * TB + 2];
 };
 struct TaskSmem {
-  union {
-    TaskChunk buf[2];   // 128-wide products
-    Stage64 blk[2];     // 64 x 64 products
-  };
+  TaskChunk buf[2];
 };
 
 union StageSmem {
@@ -113,32 +110,6 @@ __device__ __forceinline__ double load_x(const T* X, int64_t ldx, int gi, int gj
   const bool ok = gi < m && gj < n;
   const T v = X[ok ? (int64_t)gi * ldx + gj : 0];
   return ok ? (double)v : 0.0;
-}
-
-// A deferred-feedback delivery onto a single 64 x 64 target: out (+)= A B
-// with A the 64 x (64 nb) source panel and B the (64 nb) x 64 panel. The four
-// waves split the target 32 x 32 each (Acc); 64-deep blocks go global ->
-// registers -> LDS, double-buffered.
-__device__ void run_task64(const double* Ap, int64_t lda, const double* Bp, int64_t ldb,
-                           double* out, int64_t ldo, int nb, int ow, TaskSmem& sm) {
-  Acc acc;
-  acc.zero();
-  if (!ow) acc_add_from(acc, out, ldo);
-  double ra[16], rb[16];
-  load_blk(Ap, lda, ra);
-  load_blk(Bp, ldb, rb);
-  for (int b = 0; b < nb; ++b) {
-    Stage64& st = sm.blk[b & 1];
-    put_a(st, ra);
-    put_b(st, rb);
-    __syncthreads();
-    if (b + 1 < nb) {
-      load_blk(Ap + (int64_t)(b + 1) * TB, lda, ra);
-      load_blk(Bp + (int64_t)(b + 1) * TB * ldb, ldb, rb);
-    }
-    mma_blk(acc, st);
-  }
-  acc_store(acc, out, ldo, 1.0);
 }
 
 // Operands of one delivery (uniform over the work group): out (+)= A B with
@@ -175,12 +146,16 @@ __device__ __forceinline__ TaskOp task_op(const StageArgs& a, int4 tk) {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// Load instructions per wave for one chunk of T: eight right-operand rows and
+// 4 nr left-operand row blocks.
+__device__ __forceinline__ int task_loads(const TaskOp& T) { return 8 + 4 * T.nr; }
+
 // Chunk c of task T into d: wave w moves the left-operand row blocks
-// j = w + 4i (rows 4j .. 4j+3) and the right-operand rows k = w + 4i,
-// i = 0..7, sixteen 1 KB direct global -> LDS loads in all. Lane l of a
-// left-operand load takes the 16-byte piece (l & 15) ^ (l >> 4) of row
-// 4j + (l >> 4); rows and columns past the target are read from a clamped
-// address (never used).
+// j = w + 4i (rows 4j .. 4j+3, i < 4 nr) and the right-operand rows k = w + 4i
+// (i < 8), each a 1 KB direct global -> LDS load. Lane l of a left-operand
+// load takes the 16-byte piece (l & 15) ^ (l >> 4) of row 4j + (l >> 4); of a
+// right-operand load the columns 2l, 2l+1 (clamped to the target: never used
+// past it).
 __device__ __forceinline__ void task_issue(const TaskOp& T, int c, TaskChunk& d, int w, int l,
                                            int64_t ldb) {
   const int ar = l >> 4, ap = (l & 15) ^ ar;
@@ -189,22 +164,38 @@ __device__ __forceinline__ void task_issue(const TaskOp& T, int c, TaskChunk& d,
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const int j = w + 4 * i;
-    const double* pa = T.A + (int64_t)min(4 * j + ar, TB * T.nr - 1) * T.lda + 2 * ap + k0;
-    __builtin_amdgcn_global_load_lds((const void*)pa, (lds_void*)&d.a[j][0], 16, 0, 0);
+    if (i < 4 * T.nr) {
+      const double* pa = T.A + (int64_t)(4 * j + ar) * T.lda + 2 * ap + k0;
+      __builtin_amdgcn_global_load_lds((const void*)pa, (lds_void*)&d.a[j][0], 16, 0, 0);
+    }
     __builtin_amdgcn_global_load_lds((const void*)(pb + j * ldb), (lds_void*)&d.b[j][0], 16, 0, 0);
   }
 }
 
-// Accumulator of wave (qr, qc): the old target values (a delivery that adds)
-// or zero (one that overwrites, or a quadrant outside the target).
-__device__ __forceinline__ void task_init(d4 (&acc)[4][4], const TaskOp& T, int qr, int qc, int l,
+// The part of a (64 nr) x (64 nc) target that wave w computes, as NI x NJ
+// MFMA blocks of 16 x 16 from row rb and column cb:
+//   2 x 2 tiles: 64 x 64 quadrant (w >> 1, w & 1)      NI = NJ = 4
+//   2 x 1 tiles: rows 32 w .. 32 w + 31, all 64 columns NI = 2, NJ = 4
+//   1 x 2 tiles: all 64 rows, columns 32 w .. 32 w + 31 NI = 4, NJ = 2
+//   1 x 1 tile : 32 x 32 quadrant (w >> 1, w & 1)      NI = NJ = 2
+__device__ __forceinline__ void task_part(const TaskOp& T, int w, int& rb, int& cb) {
+  if (T.nr == 2 && T.nc == 2) { rb = 64 * (w >> 1); cb = 64 * (w & 1); }
+  else if (T.nr == 2) { rb = 32 * w; cb = 0; }
+  else if (T.nc == 2) { rb = 0; cb = 32 * w; }
+  else { rb = 32 * (w >> 1); cb = 32 * (w & 1); }
+}
+
+// Accumulators of the wave's part: the old target values (a delivery that
+// adds) or zero (one that overwrites).
+template <int NI, int NJ>
+__device__ __forceinline__ void task_init(d4 (&acc)[4][4], const TaskOp& T, int rb, int cb, int l,
                                           int64_t np) {
-  if (qr < T.nr && qc < T.nc && !T.ow) {
-    const double* o = T.out + (int64_t)(TB * qr) * np + TB * qc + (int64_t)(l >> 4) * np + (l & 15);
+  if (!T.ow) {
+    const double* o = T.out + (int64_t)(rb + (l >> 4)) * np + cb + (l & 15);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[i][j][r] = o[(int64_t)(16 * i + 4 * r) * np + 16 * j];
     // the accumulators are complete before the chunk loop (so that no wait
@@ -212,103 +203,113 @@ __device__ __forceinline__ void task_init(d4 (&acc)[4][4], const TaskOp& T, int 
     __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
+      for (int j = 0; j < NJ; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
   }
 }
 
-__device__ __forceinline__ void task_store(const d4 (&acc)[4][4], const TaskOp& T, int qr, int qc,
+template <int NI, int NJ>
+__device__ __forceinline__ void task_store(const d4 (&acc)[4][4], const TaskOp& T, int rb, int cb,
                                            int l, int64_t np) {
-  if (qr < T.nr && qc < T.nc) {
-    double* o = T.out + (int64_t)(TB * qr) * np + TB * qc + (int64_t)(l >> 4) * np + (l & 15);
+  double* o = T.out + (int64_t)(rb + (l >> 4)) * np + cb + (l & 15);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * np + 16 * j] = acc[i][j][r];
+      for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * np + 16 * j] = acc[i][j][r];
+}
+
+// One staged chunk on MFMA: acc[i][j] += A(rows rb + 16 i ..) B(cols cb + 16 j ..).
+template <int NI, int NJ>
+__device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, int rb, int cb, int l) {
+  const int r0 = l & 15;
+#pragma unroll
+  for (int kk = 0; kk < KQ / 4; ++kk) {
+    const int k = 4 * kk + (l >> 4), kp = 2 * kk + (l >> 5), e = (l >> 4) & 1;
+    const int rr = r0 & 3, ao = KQ * rr + 2 * (kp ^ rr) + e;
+    double av[NI], bv[NJ];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) av[i] = st.a[(rb + 16 * i + r0) >> 2][ao];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) bv[j] = st.b[k][cb + 16 * j + r0];
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[i], bv[j], acc[i][j], 0, 0, 0);
   }
 }
 
-// A run of deliveries with a 128-wide target (nr or nc = 2), streamed
-// through one double-buffered pipeline: the first chunk of the next task is
-// loaded while the last chunk of the current one is on MFMA, so tasks follow
-// each other without a pipeline drain. Wave w owns the 64 x 64 output
-// quadrant (w >> 1, w & 1) as 4 x 4 MFMA blocks; every wave multiplies (a
-// quadrant outside the target works on the clamped copies and is not
-// stored), which keeps the accumulators in the MFMA registers.
+// A run of n deliveries of one target shape (NI x NJ blocks per wave),
+// streamed through one double-buffered pipeline: the first chunk of the next
+// delivery is loaded while the last chunk of the current one is on MFMA, so
+// deliveries follow each other without a pipeline drain. Every wave has a
+// part of every target (task_part).
+template <int NI, int NJ>
 __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& sm) {
+  constexpr int NR = NI == 4 && NJ == 4 ? 2 : NI == 2 && NJ == 4 ? 2 : 1;  // target rows in tiles
+  constexpr int NL = 8 + 4 * NR;  // load instructions per wave and chunk
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
-  const int qr = w >> 1, qc = w & 1;
   const int64_t np = a.np;
-  const int r0 = l & 15, cb0 = TB * qc + (l & 15);
   d4 acc[4][4];
   TaskOp T = task_op(a, tk[0]);
   TaskOp Tn = T;
+  int rb, cb;
+  task_part(T, w, rb, cb);
   task_issue(T, 0, sm.buf[0], w, l, np);
-  task_init(acc, T, qr, qc, l, np);
+  task_init<NI, NJ>(acc, T, rb, cb, l, np);
   int idx = 0, c = 0, p = 0;
   for (;;) {
     const bool last = c + 1 == T.nch;
     if (!last) {
       task_issue(T, c + 1, sm.buf[p ^ 1], w, l, np);
-      __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16): chunk c has landed
     } else if (idx + 1 < n) {
       Tn = task_op(a, tk[idx + 1]);
       task_issue(Tn, 0, sm.buf[p ^ 1], w, l, np);
-      __builtin_amdgcn_s_waitcnt(0x4f70);
+    }
+    // chunk c has landed
+    if (!last || idx + 1 < n) {
+      if constexpr (NL == 16) __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16)
+      else __builtin_amdgcn_s_waitcnt(0x0f7c);                     // vmcnt(12)
     } else {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
     // a bare barrier: the wait above already covers this wave's part of
     // chunk c, and a fenced barrier would also wait for the next chunk
     asm volatile("s_barrier" ::: "memory");
-    const TaskChunk& st = sm.buf[p];
-#pragma unroll
-    for (int kk = 0; kk < KQ / 4; ++kk) {
-      const int k = 4 * kk + (l >> 4), kp = 2 * kk + (l >> 5), e = (l >> 4) & 1;
-      const int rr = r0 & 3, ao = KQ * rr + 2 * (kp ^ rr) + e;
-      double av[4], bv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        av[i] = st.a[(TB * qr + 16 * i + r0) >> 2][ao];
-        bv[i] = st.b[k][cb0 + 16 * i];
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
+    task_mma<NI, NJ>(acc, sm.buf[p], rb, cb, l);
     // buffer p is refilled next: every wave's reads of it are complete
     // before the barrier, while the next chunk stays in flight
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     p ^= 1;
     if (last) {
-      task_store(acc, T, qr, qc, l, np);
+      task_store<NI, NJ>(acc, T, rb, cb, l, np);
       if (++idx == n) break;
       T = Tn;
       c = 0;
-      task_init(acc, T, qr, qc, l, np);
+      task_init<NI, NJ>(acc, T, rb, cb, l, np);
     } else {
       ++c;
     }
   }
 }
 
-// One bin of a launch's deliveries, bin = {first task, streamed count |
-// single-tile count << 16}: the 128-wide ones first through the stream,
-// the single-tile ones after it.
-__device__ void run_bin(const StageArgs& a, int2 bin, TaskSmem& sm) {
+// One bin of a launch's deliveries, bin = {first task, n22 | n21 << 16,
+// n12 | n11 << 16, 0}: the counts of 2 x 2, 2 x 1, 1 x 2 and 1 x 1 targets,
+// the tasks grouped in that order; each group is one stream.
+__device__ void run_bin(const StageArgs& a, int4 bin, TaskSmem& sm) {
   const int4* tk = a.tasks + bin.x;
-  const int ns = bin.y & 0xffff, n1 = bin.y >> 16;
-  if (ns > 0) run_stream(a, tk, ns, sm);
-  for (int i = 0; i < n1; ++i) {
-    if (ns > 0 || i > 0) __syncthreads();  // the staging buffers are reused
-    const TaskOp T = task_op(a, tk[ns + i]);
-    run_task64(T.A, T.lda, T.B, a.np, T.out, a.np, T.nch / (TB / KQ), T.ow, sm);
-  }
+  const int n4 = bin.y & 0xffff, n21 = bin.y >> 16, n12 = bin.z & 0xffff, n11 = bin.z >> 16;
+  bool busy = false;  // a group before this one used the staging buffers
+  if (n4) { run_stream<4, 4>(a, tk, n4, sm); busy = true; }
+  tk += n4;
+  if (n21) { if (busy) __syncthreads(); run_stream<2, 4>(a, tk, n21, sm); busy = true; }
+  tk += n21;
+  if (n12) { if (busy) __syncthreads(); run_stream<4, 2>(a, tk, n12, sm); busy = true; }
+  tk += n12;
+  if (n11) { if (busy) __syncthreads(); run_stream<2, 2>(a, tk, n11, sm); }
 }
 
 // acc += A (16 x K) B (K x 16) on MFMA, both operands row-major in LDS with
@@ -847,26 +848,31 @@ void schedule_tasks(int MT, int NTt, int g, std::vector<int4>& all, std::vector<
 }
 
 // Bins of a stage: one per compute unit, filled longest-processing-time
-// first with an estimated cost per task (in microseconds: about 3.6 per
-// 32-deep chunk of a 128-wide product, 5 per 64-deep block of a single-tile
-// one, plus a start cost), so that the bins finish close together; a work
-// group per non-empty bin, after the sweeps. The first units - nsweep bins
-// start beside the sweeps; the others only when a sweep is done, so they
-// start loaded with its duration (and stay empty when the work fits beside
-// the sweeps). In a bin the 128-wide tasks come first (they share one
-// streamed pipeline), the single-tile ones after them.
-constexpr double kSweepCost = 45.0;  // one tile sweep, microseconds
-void pack_bins(int MT, int NTt, int units, std::vector<int4>& all, const std::vector<int>& off,
-               std::vector<int2>& bins, std::vector<int>& boff) {
+// first with an estimated cost per task (microseconds per 32-deep chunk by
+// target size, plus a start cost that is larger when the old target values
+// are read), so that the bins finish close together; a work group per
+// non-empty bin, after the sweeps. The first units - nsweep bins start
+// beside the sweeps; the others only when a sweep is done, so they start
+// loaded with its duration (and stay empty when the work fits beside the
+// sweeps).
+constexpr double kSweepCost = 45.0;   // one tile sweep
+constexpr double kChunk4 = 5.0;       // 32-deep chunk onto 2 x 2 tiles
+constexpr double kChunk2 = 3.0;       // onto 2 x 1 or 1 x 2 tiles
+constexpr double kChunk1 = 1.8;       // onto one tile
+constexpr double kStartOw = 1.0;      // a delivery that overwrites
+constexpr double kStartAdd = 3.0;     // a delivery that adds to the old values
+gptq2d_status pack_bins(int MT, int NTt, int units, std::vector<int4>& all,
+                        const std::vector<int>& off, std::vector<int4>& bins, std::vector<int>& boff) {
   const int S = MT + NTt - 1;
   bins.clear();
   boff.assign(S + 1, 0);
   std::vector<int4> out;
   out.reserve(all.size());
-  auto small = [](const int4& x) { return ((x.x >> 2) & 3) == 0; };
-  auto cost = [&](const int4& x) {
+  auto cost = [](const int4& x) {
     const int K = (x.w >> 16) - (x.w & 0xffff);
-    return small(x) ? 2.0 + 5.0 * K : 1.0 + 3.6 * 2 * K;
+    const int tiles = (((x.x >> 2) & 1) + 1) * (((x.x >> 3) & 1) + 1);
+    const double chunk = tiles == 4 ? kChunk4 : tiles == 2 ? kChunk2 : kChunk1;
+    return ((x.x >> 1) & 1 ? kStartOw : kStartAdd) + chunk * (TB / KQ) * K;
   };
   for (int k = 0; k < S; ++k) {
     boff[k] = (int)bins.size();
@@ -894,17 +900,25 @@ void pack_bins(int MT, int NTt, int units, std::vector<int4>& all, const std::ve
     const int base = (int)out.size();
     for (int b = 0; b < nb; ++b) {
       if (member[b].empty()) continue;
+      // grouped by target shape: 2 x 2, 2 x 1, 1 x 2, 1 x 1
+      if (member[b].size() > 0xffff) {
+        set_error("delivery plan: too many products in one bin");
+        return GPTQ2D_ERR_INVALID_ARG;
+      }
+      int cnt[4] = {0, 0, 0, 0};
       const int first = (int)out.size() - base;
-      int ns = 0, n1 = 0;
-      for (int i : member[b])
-        if (!small(all[i])) out.push_back(all[i]), ++ns;
-      for (int i : member[b])
-        if (small(all[i])) out.push_back(all[i]), ++n1;
-      bins.push_back(make_int2(first, ns | (n1 << 16)));
+      for (int g = 0; g < 4; ++g)
+        for (int i : member[b]) {
+          const int nr = ((all[i].x >> 2) & 1) + 1, nc = ((all[i].x >> 3) & 1) + 1;
+          const int sh = nr == 2 ? (nc == 2 ? 0 : 1) : (nc == 2 ? 2 : 3);
+          if (sh == g) out.push_back(all[i]), ++cnt[g];
+        }
+      bins.push_back(make_int4(first, cnt[0] | (cnt[1] << 16), cnt[2] | (cnt[3] << 16), 0));
     }
   }
   boff[S] = (int)bins.size();
   all.swap(out);
+  return GPTQ2D_OK;
 }
 
 void free_schedule(Schedule& sc) {
@@ -923,18 +937,19 @@ gptq2d_status build_schedule(Factors& f, int g) {
   if (hipDeviceGetAttribute(&units, hipDeviceAttributeMultiprocessorCount, f.device) != hipSuccess ||
       units <= 0)
     units = 256;
-  std::vector<int2> bins;
+  std::vector<int4> bins;
   std::vector<int> boff;
-  pack_bins(f.MT, f.NT, units, all, off, bins, boff);
+  const gptq2d_status st = pack_bins(f.MT, f.NT, units, all, off, bins, boff);
+  if (st != GPTQ2D_OK) return st;
   free_schedule(f.sched);
   if (!all.empty()) {
     hipError_t e = hipMalloc(&f.sched.d_tasks, all.size() * sizeof(int4));
     if (e != hipSuccess) return hip_fail(e, "schedule allocation");
     e = hipMemcpy(f.sched.d_tasks, all.data(), all.size() * sizeof(int4), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "schedule upload");
-    e = hipMalloc(&f.sched.d_bins, bins.size() * sizeof(int2));
+    e = hipMalloc(&f.sched.d_bins, bins.size() * sizeof(int4));
     if (e != hipSuccess) return hip_fail(e, "schedule allocation");
-    e = hipMemcpy(f.sched.d_bins, bins.data(), bins.size() * sizeof(int2), hipMemcpyHostToDevice);
+    e = hipMemcpy(f.sched.d_bins, bins.data(), bins.size() * sizeof(int4), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "schedule upload");
   }
   f.sched.g = g;
