@@ -144,11 +144,13 @@ __device__ void gram_tile(const Side& sd, const T* S, int64_t ld, int bp, int bq
       }
 }
 
+// Sides in a Gram launch: side 0 if bit 0 of `sides` is set, side 1 if bit
+// 1 is; the grid holds the lower tiles of the first, then of the second.
 template <typename T>
 __global__ __launch_bounds__(NT) void k_gram(FacArgs f, const T* A, int64_t lda, const T* B,
-                                             int64_t ldb) {
+                                             int64_t ldb, int sides) {
   __shared__ Stage64 st;
-  const int t0 = f.s[0].nb * (f.s[0].nb + 1) / 2;
+  const int t0 = (sides & 1) ? f.s[0].nb * (f.s[0].nb + 1) / 2 : 0;
   int bp, bq;
   if ((int)blockIdx.x < t0) {
     tri_index(blockIdx.x, bp, bq);
@@ -157,6 +159,162 @@ __global__ __launch_bounds__(NT) void k_gram(FacArgs f, const T* A, int64_t lda,
     tri_index(blockIdx.x - t0, bp, bq);
     gram_tile<T, 1>(f.s[1], B, ldb, bp, bq, st);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Gram of a side whose dimension is a multiple of 128, in two steps.
+//
+// k_gram_prep writes, widened to fp64, the row-major panel S (d x d, row
+// stride d) whose rows are the reversed Gram indices: S[p][k] = A[k][d-1-p]
+// (side 0, a transpose through LDS) or B[d-1-p][k] (side 1). The panel lives
+// in the side's inverse buffer, which the factorisation fills only later.
+//
+// k_gram128 then forms Gr[p][q] = sum_k S[p][k] S[q][k] on the lower
+// 128 x 128 tiles: four waves, each a 64 x 64 quadrant as 4 x 4 MFMA blocks
+// (the upper quadrant of a diagonal tile is computed but not stored), the
+// 32-deep chunks of both 128-row panels streamed by direct global -> LDS
+// loads into double buffers (the same layout as the delivery products: row
+// blocks of four, 16-byte pieces XOR-permuted by the row's position in the
+// block, 64 bytes of padding per block).
+// ---------------------------------------------------------------------------
+
+constexpr int GQ = 32;           // chunk depth
+constexpr int GA = 4 * GQ + 8;   // doubles per 4-row block
+struct GramChunk {
+  double a[32][GA];   // rows 128 bp ..
+  double b[32][GA];   // rows 128 bq ..
+};
+
+template <typename T>
+__global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f, const T* A, int64_t lda, const T* B,
+                                                  int64_t ldb, int sides) {
+  __shared__ double tile[TB][TB + 1];
+  const int n0 = (sides & 1) ? (f.s[0].d / TB) * (f.s[0].d / TB) : 0;
+  int b = blockIdx.x;
+  const int side = b < n0 ? 0 : 1;
+  if (side == 1) b -= n0;
+  const Side& sd = f.s[side];
+  const int d = sd.d, nt = d / TB;
+  const int i0 = (b / nt) * TB, k0 = (b % nt) * TB;  // S rows i0.., columns k0..
+  double* S = sd.li;
+  const int t = threadIdx.x;
+  if (side == 0) {
+    // A rows k0 + r, columns d-1-(i0+63) .. d-1-i0 (ascending), coalesced
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int e = t + NT * u, r = e >> 6, c = e & 63;  // c: column offset in A
+      tile[r][c] = (double)A[(int64_t)(k0 + r) * lda + (d - i0 - TB) + c];
+    }
+    __syncthreads();
+    // S[i0 + i][k0 + k] = A[k0 + k][d-1-(i0+i)] = tile[k][63 - i]
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int e = t + NT * u, i = e >> 6, k = e & 63;
+      S[(int64_t)(i0 + i) * d + k0 + k] = tile[k][TB - 1 - i];
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int e = t + NT * u, i = e >> 6, k = e & 63;
+      S[(int64_t)(i0 + i) * d + k0 + k] = (double)B[(int64_t)(d - 1 - (i0 + i)) * ldb + k0 + k];
+    }
+  }
+}
+
+__device__ __forceinline__ void gram_issue(const double* Sp, const double* Sq, int64_t ld, int c,
+                                           GramChunk& g, int w, int l) {
+  typedef __attribute__((address_space(3))) void lds_v;
+  const int ar = l >> 4, ap = (l & 15) ^ ar;
+  const int64_t k0 = (int64_t)c * GQ + 2 * ap;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int j = w + 4 * i;
+    const int64_t ro = (int64_t)(4 * j + ar) * ld + k0;
+    __builtin_amdgcn_global_load_lds((const void*)(Sp + ro), (lds_v*)&g.a[j][0], 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(Sq + ro), (lds_v*)&g.b[j][0], 16, 0, 0);
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_gram128(FacArgs f, int sides) {
+  __shared__ GramChunk buf[2];
+  const int nt0 = f.s[0].d / 128;
+  const int t0 = (sides & 1) ? nt0 * (nt0 + 1) / 2 : 0;
+  // work groups are dealt round-robin to the eight L2 domains (XCDs): give
+  // each domain a contiguous run of tiles, so that the tiles it runs at the
+  // same time share their row panel (tri_index enumerates row by row)
+  // (domain x holds the blocks b = x mod 8, q of them, and gets the tiles
+  // from x q + min(x, r) on, with q, r the quotient and remainder by 8)
+  const int ntile = gridDim.x, q8 = ntile / 8, r8 = ntile % 8;
+  const int x = blockIdx.x % 8;
+  int b = x * q8 + min(x, r8) + (int)blockIdx.x / 8;
+  const int side = b < t0 ? 0 : 1;
+  if (side == 1) b -= t0;
+  const Side& sd = f.s[side];
+  int bp, bq;
+  tri_index(b, bp, bq);
+  const int d = sd.d;
+  const double* Sp = sd.li + (int64_t)(128 * bp) * d;
+  const double* Sq = sd.li + (int64_t)(128 * bq) * d;
+  const int t = threadIdx.x, w = t >> 6, l = t & 63;
+  const int qr = w >> 1, qc = w & 1, r0 = l & 15;
+  d4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
+  const int nch = d / GQ;
+  gram_issue(Sp, Sq, d, 0, buf[0], w, l);
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) {
+      gram_issue(Sp, Sq, d, c + 1, buf[(c + 1) & 1], w, l);
+      __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16): chunk c has landed
+    } else {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+    }
+    asm volatile("s_barrier" ::: "memory");  // the wait above covers this wave's part
+    const GramChunk& st = buf[c & 1];
+    // operands of k-step kk + 1 are read while kk is on MFMA (two register
+    // sets), the reads spread between the MFMAs
+    double av[2][4], bv[2][4];
+    const int rr = r0 & 3;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int ao = GQ * rr + 2 * ((l >> 5) ^ rr) + ((l >> 4) & 1);
+      av[0][i] = st.a[(64 * qr + 16 * i + r0) >> 2][ao];
+      bv[0][i] = st.b[(64 * qc + 16 * i + r0) >> 2][ao];
+    }
+#pragma unroll
+    for (int kk = 0; kk < GQ / 4; ++kk) {
+      const int cur = kk & 1, nx = cur ^ 1;
+      if (kk + 1 < GQ / 4) {
+        const int kp = 2 * (kk + 1) + (l >> 5), ao = GQ * rr + 2 * (kp ^ rr) + ((l >> 4) & 1);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          av[nx][i] = st.a[(64 * qr + 16 * i + r0) >> 2][ao];
+          bv[nx][i] = st.b[(64 * qc + 16 * i + r0) >> 2][ao];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[cur][i], bv[cur][j], acc[i][j], 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two MFMAs
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // buffer refilled next
+  }
+  if (bp == bq && qr < qc) return;  // upper quadrant of a diagonal tile
+  double* o = sd.gr + (int64_t)(128 * bp + 64 * qr + (l >> 4)) * sd.dp + 128 * bq + 64 * qc + (l & 15);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * sd.dp + 16 * j] = acc[i][j][r];
 }
 
 // ---------------------------------------------------------------------------
@@ -618,12 +776,38 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
   const int nb0 = a.s[0].nb, nb1 = a.s[1].nb, nbmax = nb0 > nb1 ? nb0 : nb1;
   const int tri = nb0 * (nb0 + 1) / 2 + nb1 * (nb1 + 1) / 2;
   hipLaunchKernelGGL(k_zero_int, dim3(1), dim3(64), 0, s, f.flags, 1);
-  if (dt == GPTQ2D_F32)
-    hipLaunchKernelGGL(k_gram<float>, dim3(tri), dim3(NT), 0, s, a, (const float*)A, lda,
-                       (const float*)B, ldb);
-  else
-    hipLaunchKernelGGL(k_gram<double>, dim3(tri), dim3(NT), 0, s, a, (const double*)A, lda,
-                       (const double*)B, ldb);
+  // Gram: sides whose dimension is a multiple of 128 through the prepared
+  // panel and 128 x 128 tiles, the others with 64 x 64 tiles straight from
+  // the input
+  int fast = 0, slow = 0, nprep = 0, n128 = 0, nslow = 0;
+  for (int sd = 0; sd < 2; ++sd) {
+    const int d = a.s[sd].d, nb = a.s[sd].nb;
+    if (d % 128 == 0) {
+      fast |= 1 << sd;
+      nprep += (d / TB) * (d / TB);
+      n128 += (d / 128) * (d / 128 + 1) / 2;
+    } else {
+      slow |= 1 << sd;
+      nslow += nb * (nb + 1) / 2;
+    }
+  }
+  if (fast) {
+    if (dt == GPTQ2D_F32)
+      hipLaunchKernelGGL(k_gram_prep<float>, dim3(nprep), dim3(NT), 0, s, a, (const float*)A, lda,
+                         (const float*)B, ldb, fast);
+    else
+      hipLaunchKernelGGL(k_gram_prep<double>, dim3(nprep), dim3(NT), 0, s, a, (const double*)A,
+                         lda, (const double*)B, ldb, fast);
+    hipLaunchKernelGGL(k_gram128, dim3(n128), dim3(NT), 0, s, a, fast);
+  }
+  if (slow) {
+    if (dt == GPTQ2D_F32)
+      hipLaunchKernelGGL(k_gram<float>, dim3(nslow), dim3(NT), 0, s, a, (const float*)A, lda,
+                         (const float*)B, ldb, slow);
+    else
+      hipLaunchKernelGGL(k_gram<double>, dim3(nslow), dim3(NT), 0, s, a, (const double*)A, lda,
+                         (const double*)B, ldb, slow);
+  }
   auto update = [&](const UpdRange& r, hipStream_t st) {
     const int nu = h_upd_count(nb0, r) + h_upd_count(nb1, r);
     if (nu > 0) hipLaunchKernelGGL(k_update, dim3(nu), dim3(NT), 0, st, a, r);

@@ -222,23 +222,39 @@ __device__ __forceinline__ void task_store(const d4 (&acc)[4][4], const TaskOp& 
 }
 
 // One staged chunk on MFMA: acc[i][j] += A(rows rb + 16 i ..) B(cols cb + 16 j ..).
+// The operands of k-step kk + 1 are read while kk is on MFMA (two register
+// sets), the reads spread between the MFMAs.
 template <int NI, int NJ>
 __device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, int rb, int cb, int l) {
-  const int r0 = l & 15;
+  const int r0 = l & 15, rr = r0 & 3;
+  double av[2][NI], bv[2][NJ];
 #pragma unroll
-  for (int kk = 0; kk < KQ / 4; ++kk) {
-    const int k = 4 * kk + (l >> 4), kp = 2 * kk + (l >> 5), e = (l >> 4) & 1;
-    const int rr = r0 & 3, ao = KQ * rr + 2 * (kp ^ rr) + e;
-    double av[NI], bv[NJ];
+  for (int kk = -1; kk < KQ / 4; ++kk) {
+    const int nx = (kk + 1) & 1;
+    if (kk + 1 < KQ / 4) {
+      const int k = 4 * (kk + 1) + (l >> 4), kp = 2 * (kk + 1) + (l >> 5), e = (l >> 4) & 1;
+      const int ao = KQ * rr + 2 * (kp ^ rr) + e;
 #pragma unroll
-    for (int i = 0; i < NI; ++i) av[i] = st.a[(rb + 16 * i + r0) >> 2][ao];
+      for (int i = 0; i < NI; ++i) av[nx][i] = st.a[(rb + 16 * i + r0) >> 2][ao];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) bv[j] = st.b[k][cb + 16 * j + r0];
+      for (int j = 0; j < NJ; ++j) bv[nx][j] = st.b[k][cb + 16 * j + r0];
+    }
+    if (kk >= 0) {
+      const int cur = kk & 1;
 #pragma unroll
-    for (int i = 0; i < NI; ++i)
+      for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[i], bv[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < NJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[cur][i], bv[cur][j], acc[i][j], 0, 0, 0);
+      if (kk + 1 < KQ / 4) {
+        constexpr int NM = NI * NJ, NR = NI + NJ;  // MFMAs and reads per k-step
+#pragma unroll
+        for (int u = 0; u < NR; ++u) {
+          __builtin_amdgcn_sched_group_barrier(0x008, NM / NR > 0 ? NM / NR : 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+      }
+    }
   }
 }
 
