@@ -575,13 +575,14 @@ __global__ __launch_bounds__(NT) void k_panel(FacArgs f, int kb) {
 
 struct UpdRange {
   int qa, qb, sa, sb, k0, k1;
+  int j0;  // S columns from j0 on (jb in [j0, k1))
 };
 
 __device__ __forceinline__ void upd_counts(const Side& sd, const UpdRange& r, int& nq, int& ns) {
   nq = ns = 0;
   if (r.k0 >= sd.nb) return;
   for (int bj = r.qa; bj < min(r.qb, sd.nb); ++bj) nq += sd.nb - bj;
-  ns = max(0, min(r.sb, sd.nb) - r.sa) * min(r.k1, sd.nb);
+  ns = max(0, min(r.sb, sd.nb) - r.sa) * max(0, min(r.k1, sd.nb) - r.j0);
 }
 
 // acc += sum over 64-deep blocks b of A_b op(B_b), A_b at pa + b*sa_, B_b at
@@ -645,7 +646,7 @@ __global__ __launch_bounds__(NT) void k_update(FacArgs f, UpdRange r) {
           out[(int64_t)acc_row(u, q) * sd.dp + acc_col(v)] = old[u][v][q] - acc.t[2 * u + v][q];
   } else {
     b -= nq;
-    const int ib = r.sa + b / k1, jb = b % k1;
+    const int ib = r.sa + b / (k1 - r.j0), jb = r.j0 + b % (k1 - r.j0);
     const int kb0 = max(r.k0, jb);
     double* out = sd.li + (int64_t)ib * TB * sd.dp + (int64_t)jb * TB;
     if (jb < r.k0) acc_add_from(acc, out, sd.dp);
@@ -653,6 +654,161 @@ __global__ __launch_bounds__(NT) void k_update(FacArgs f, UpdRange r) {
                    sd.li + (int64_t)kb0 * TB * sd.dp + (int64_t)jb * TB, sd.dp, (int64_t)TB * sd.dp,
                    k1 - kb0, st);
     acc_store(acc, out, sd.dp, 1.0);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The far part of a group's trailing update on 128 x 128 tiles, for the
+// group of panels g0 .. g1-1 and the block rows / columns from g2 on (g0, g2
+// even):
+//   Q tiles (BI >= BJ >= g2/2):  Q -= Lc[BI][g0:g1] Lc[BJ][g0:g1]^T
+//   S tiles (BI >= g2/2, BJ < g0/2): S += Lc[BI][g0:g1] Li[g0:g1][BJ]
+// with the same meaning as in k_update (the group's own S columns stay
+// there). Four waves, each a 64 x 64 quadrant as 4 x 4 MFMA blocks; the
+// accumulators start from the old values (the left operand enters negated
+// for Q); 32-deep chunks of both operands by direct global -> LDS loads,
+// double-buffered, in the layouts of the Gram tiles (rows with a contiguous
+// contraction index) and, for the right operand of S, rows of Li (b[k][j]).
+// A tile past the last block row / column (odd block count) is loaded from
+// clamped rows and its missing quadrants are not stored.
+// ---------------------------------------------------------------------------
+
+struct UpdChunk {
+  double a[32][GA];
+  union {
+    double bt[32][GA];         // right operand given as rows (Q)
+    double b[GQ][2 * TB + 2];  // right operand rows k (S)
+  };
+};
+
+template <int BT>
+__device__ __forceinline__ void upd_issue(const double* Ap, int64_t lda, const double* Bp, int64_t ldb,
+                                          int c, int nr, int nc, UpdChunk& d, int w, int l) {
+  typedef __attribute__((address_space(3))) void lds_v;
+  const int ar = l >> 4, ap = (l & 15) ^ ar;
+  const int64_t k0 = (int64_t)c * GQ;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int j = w + 4 * i;
+    const double* pa = Ap + (int64_t)min(4 * j + ar, TB * nr - 1) * lda + k0 + 2 * ap;
+    __builtin_amdgcn_global_load_lds((const void*)pa, (lds_v*)&d.a[j][0], 16, 0, 0);
+    if (BT) {
+      const double* pb = Bp + (int64_t)min(4 * j + ar, TB * nc - 1) * ldb + k0 + 2 * ap;
+      __builtin_amdgcn_global_load_lds((const void*)pb, (lds_v*)&d.bt[j][0], 16, 0, 0);
+    } else {
+      const double* pb = Bp + (k0 + j) * ldb + min(2 * l, TB * nc - 2);
+      __builtin_amdgcn_global_load_lds((const void*)pb, (lds_v*)&d.b[j][0], 16, 0, 0);
+    }
+  }
+}
+
+template <int BT>
+__device__ void upd_tile(double* out, int64_t ldo, const double* Ap, int64_t lda, const double* Bp,
+                         int64_t ldb, int K, int nr, int nc, bool diag, UpdChunk* buf) {
+  const int t = threadIdx.x, w = t >> 6, l = t & 63;
+  const int qr = w >> 1, qc = w & 1, r0 = l & 15, rr = r0 & 3;
+  const bool mine = qr < nr && qc < nc && !(diag && qr < qc);
+  const double sgn = BT ? -1.0 : 1.0;
+  double* o = out + (int64_t)(64 * qr + (l >> 4)) * ldo + 64 * qc + (l & 15);
+  d4 acc[4][4];
+  upd_issue<BT>(Ap, lda, Bp, ldb, 0, nr, nc, buf[0], w, l);
+  if (mine) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[i][j][r] = o[(int64_t)(16 * i + 4 * r) * ldo + 16 * j];
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): no wait for them inside the loop
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
+  }
+  const int nch = K / GQ;
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) {
+      upd_issue<BT>(Ap, lda, Bp, ldb, c + 1, nr, nc, buf[(c + 1) & 1], w, l);
+      __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16): chunk c has landed
+    } else {
+      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+    }
+    asm volatile("s_barrier" ::: "memory");  // the wait above covers this wave's part
+    const UpdChunk& st = buf[c & 1];
+    double av[2][4], bv[2][4];
+#pragma unroll
+    for (int kk = -1; kk < GQ / 4; ++kk) {
+      const int nx = (kk + 1) & 1;
+      if (kk + 1 < GQ / 4) {
+        const int k = 4 * (kk + 1) + (l >> 4), kp = 2 * (kk + 1) + (l >> 5);
+        const int ao = GQ * rr + 2 * (kp ^ rr) + ((l >> 4) & 1);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          av[nx][i] = sgn * st.a[(64 * qr + 16 * i + r0) >> 2][ao];
+          bv[nx][i] = BT ? st.bt[(64 * qc + 16 * i + r0) >> 2][ao] : st.b[k][64 * qc + 16 * i + r0];
+        }
+      }
+      if (kk >= 0) {
+        const int cur = kk & 1;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[cur][i], bv[cur][j], acc[i][j], 0, 0, 0);
+        if (kk + 1 < GQ / 4) {
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+        }
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // buffer refilled next
+  }
+  if (mine) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * ldo + 16 * j] = acc[i][j][r];
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_update128(FacArgs f, int g0, int g1, int g2) {
+  __shared__ UpdChunk buf[2];
+  int b = blockIdx.x;
+  for (int s = 0; s < 2; ++s) {
+    const Side& sd = f.s[s];
+    const int nb = sd.nb;
+    if (g0 >= nb || g1 <= g0) continue;
+    const int nb2 = (nb + 1) / 2, t0 = g2 / 2;
+    if (t0 >= nb2) continue;
+    const int nq = (nb2 - t0) * (nb2 - t0 + 1) / 2, ns = (nb2 - t0) * (g0 / 2);
+    const int K = TB * (min(g1, nb) - g0);
+    const int64_t dp = sd.dp;
+    if (b < nq) {
+      int bi, bj;
+      tri_index(b, bi, bj);  // bi >= bj, relative to t0
+      const int BI = t0 + bi, BJ = t0 + bj;
+      upd_tile<1>(sd.gr + (int64_t)128 * BI * dp + 128 * BJ, dp,
+                  sd.gr + (int64_t)128 * BI * dp + TB * g0, dp,
+                  sd.gr + (int64_t)128 * BJ * dp + TB * g0, dp, K,
+                  min(2, nb - 2 * BI), min(2, nb - 2 * BJ), BI == BJ, buf);
+      return;
+    }
+    b -= nq;
+    if (b < ns) {
+      const int BI = t0 + b / (g0 / 2), BJ = b % (g0 / 2);
+      upd_tile<0>(sd.li + (int64_t)128 * BI * dp + 128 * BJ, dp,
+                  sd.gr + (int64_t)128 * BI * dp + TB * g0, dp,
+                  sd.li + (int64_t)TB * g0 * dp + 128 * BJ, dp, K,
+                  min(2, nb - 2 * BI), 2, false, buf);
+      return;
+    }
+    b -= ns;
   }
 }
 
@@ -767,7 +923,17 @@ static int h_upd_count(int nb, const UpdRange& r) {
   if (r.k0 >= nb) return 0;
   int nq = 0;
   for (int bj = r.qa; bj < std::min(r.qb, nb); ++bj) nq += nb - bj;
-  return nq + std::max(0, std::min(r.sb, nb) - r.sa) * std::min(r.k1, nb);
+  return nq + std::max(0, std::min(r.sb, nb) - r.sa) * std::max(0, std::min(r.k1, nb) - r.j0);
+}
+
+// work groups of k_update128 for one side (see there)
+static void h_far_counts(int nb, int g0, int g1, int g2, int& nq, int& ns) {
+  nq = ns = 0;
+  if (g0 >= nb || g1 <= g0) return;
+  const int nb2 = (nb + 1) / 2, t0 = g2 / 2;
+  if (t0 >= nb2) return;
+  nq = (nb2 - t0) * (nb2 - t0 + 1) / 2;
+  ns = (nb2 - t0) * (g0 / 2);
 }
 
 gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t lda,
@@ -828,19 +994,26 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
       hipLaunchKernelGGL(k_diag, dim3(2), dim3(NT), 0, s, a, kb);
       const int np_ = h_panel_count(nb0, kb) + h_panel_count(nb1, kb);
       if (np_ > 0) hipLaunchKernelGGL(k_panel, dim3(np_), dim3(NT), 0, s, a, kb);
-      if (kb + 1 < g1) update(UpdRange{kb + 1, g1, kb + 1, g1, kb, kb + 1}, s);
+      if (kb + 1 < g1) update(UpdRange{kb + 1, g1, kb + 1, g1, kb, kb + 1, 0}, s);
     }
     if (far_pending) {
       he = hipStreamWaitEvent(s, f.ev_far, 0);
       if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
       far_pending = false;
     }
-    update(UpdRange{g1, g2, g1, g2, g0, g1}, s);
+    update(UpdRange{g1, g2, g1, g2, g0, g1, 0}, s);
     if (g2 < nbmax) {
       he = hipEventRecord(f.ev_near, s);
       if (he == hipSuccess) he = hipStreamWaitEvent(f.aux, f.ev_near, 0);
       if (he != hipSuccess) return hip_fail(he, "event record / wait");
-      update(UpdRange{g2, nbmax, g2, nbmax, g0, g1}, f.aux);
+      // the bulk on 128 x 128 tiles; the inverse columns of the group
+      // itself (variable depth, first contribution overwrites) on 64 x 64
+      int fq0, fs0, fq1, fs1;
+      h_far_counts(nb0, g0, g1, g2, fq0, fs0);
+      h_far_counts(nb1, g0, g1, g2, fq1, fs1);
+      if (fq0 + fs0 + fq1 + fs1 > 0)
+        hipLaunchKernelGGL(k_update128, dim3(fq0 + fs0 + fq1 + fs1), dim3(NT), 0, f.aux, a, g0, g1, g2);
+      update(UpdRange{g2, g2, g2, nbmax, g0, g1, g0}, f.aux);
       he = hipEventRecord(f.ev_far, f.aux);
       if (he != hipSuccess) return hip_fail(he, "hipEventRecord");
       far_pending = true;
