@@ -120,8 +120,13 @@ gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
     if (he == hipSuccess) he = hipEventCreateWithFlags(&f->ev_far, hipEventDisableTiming);
     if (he != hipSuccess) st = hip_fail(he, "stream / event creation");
   }
-  if (st == GPTQ2D_OK)
-    st = build_schedule(*f, env_int("GPTQ2D_BATCH", 4));
+  if (st == GPTQ2D_OK) {
+    // far-delivery batch width in source tiles: wider batches mean fewer
+    // read-modify-writes of the feedback buffers but coarser products; five
+    // measured best from about 128 tiles per side on, four below
+    const int g = std::max(f->MT, f->NT) > 64 ? 5 : 4;
+    st = build_schedule(*f, env_int("GPTQ2D_BATCH", g));
+  }
   if (st != GPTQ2D_OK) {
     free_all(f);
     delete f;
