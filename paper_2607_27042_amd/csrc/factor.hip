@@ -403,13 +403,13 @@ __device__ __forceinline__ double bcast16(double v, int lane) {
 // every 16-lane row holds column x of the symmetric block and column x of
 // the inverse in registers, and every broadcast is a DPP broadcast of one
 // lane within the row. Pivot j:
-//   - the column j of L is broadcast: L[r][j] = S[r][j] / sqrt(S[j][j]),
-//     and written out (zeros above the diagonal) by lane j;
+//   - the column j of L is broadcast: L[r][j] = S[r][j] / sqrt(S[j][j]);
 //   - lane x's entry j becomes L[x][j] (by symmetry), and every lane
 //     subtracts L[r][j] L[x][j] from its entries r > j (right-looking
-//     Cholesky; lanes x <= j only touch columns already written out);
+//     Cholesky; entries r > x of lane x are never used again);
 //   - every lane advances the column-oriented forward substitution of
 //     L W = I with the same column: w[j] /= L[j][j], w[r] -= L[r][j] w[j].
+// At the end lane x holds row x of L (entries 0..x) and column x of W.
 __device__ void chol_inv16(double* A, int lda, double* W, int ldw, int* flags) {
   int l = threadIdx.x & 63;
   // opaque to the optimiser: keeps the per-lane set-up inside the caller's
@@ -437,21 +437,24 @@ __device__ void chol_inv16(double* A, int lda, double* W, int ldw, int* flags) {
     double lc[DS];
 #pragma unroll
     for (int r = j + 1; r < DS; ++r) lc[r] = bcast16(a[r], j) * rs;
-    if (l == j) {
-#pragma unroll
-      for (int r = 0; r < DS; ++r) A[r * lda + j] = r < j ? 0.0 : (r == j ? a[j] : lc[r]);
-    }
 #pragma unroll
     for (int r = j + 1; r < DS; ++r) {
       a[r] = fma(lc[r], na, a[r]);
       w[r] = fma(lc[r], nw, w[r]);
     }
+#ifndef G2D_NO_PIVOT_FENCE
     __builtin_amdgcn_sched_barrier(0);  // keep each pivot's broadcasts local (register pressure)
+#endif
   }
   if (bad && l == 0) raise_flag(flags, FLAG_SINGULAR);
+  // after pivot j, a[j] of lane x is L[x][j] (x >= j): each lane holds row x of
+  // the factor and column x of its inverse
   if (l < DS) {
 #pragma unroll
-    for (int r = 0; r < DS; ++r) W[r * ldw + x] = (r >= x) ? w[r] : 0.0;
+    for (int r = 0; r < DS; ++r) {
+      A[x * lda + r] = (r <= x) ? a[r] : 0.0;
+      W[r * ldw + x] = (r >= x) ? w[r] : 0.0;
+    }
   }
 }
 
