@@ -780,9 +780,7 @@ __device__ void upd_tile(double* out, int64_t ldo, const double* Ap, int64_t lda
   }
 }
 
-__global__ __launch_bounds__(NT) void k_update128(FacArgs f, int g0, int g1, int g2) {
-  __shared__ UpdChunk buf[2];
-  int b = blockIdx.x;
+__device__ void update128_tile(const FacArgs& f, int g0, int g1, int g2, int b, UpdChunk* buf) {
   for (int s = 0; s < 2; ++s) {
     const Side& sd = f.s[s];
     const int nb = sd.nb;
@@ -812,6 +810,17 @@ __global__ __launch_bounds__(NT) void k_update128(FacArgs f, int g0, int g1, int
       return;
     }
     b -= ns;
+  }
+}
+
+// ntile tiles over the grid, tile b by work group b mod gridDim.x: a grid
+// smaller than the device leaves compute units to the diagonal blocks and
+// panels that run beside it on the other stream
+__global__ __launch_bounds__(NT) void k_update128(FacArgs f, int g0, int g1, int g2, int ntile) {
+  __shared__ UpdChunk buf[2];
+  for (int b = blockIdx.x; b < ntile; b += gridDim.x) {
+    if (b != (int)blockIdx.x) __syncthreads();  // the staging buffers are reused
+    update128_tile(f, g0, g1, g2, b, buf);
   }
 }
 
@@ -1014,8 +1023,16 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
       int fq0, fs0, fq1, fs1;
       h_far_counts(nb0, g0, g1, g2, fq0, fs0);
       h_far_counts(nb1, g0, g1, g2, fq1, fs1);
-      if (fq0 + fs0 + fq1 + fs1 > 0)
-        hipLaunchKernelGGL(k_update128, dim3(fq0 + fs0 + fq1 + fs1), dim3(NT), 0, f.aux, a, g0, g1, g2);
+      const int nfar = fq0 + fs0 + fq1 + fs1;
+      if (nfar > 0) {
+        int units = 256;
+        (void)hipDeviceGetAttribute(&units, hipDeviceAttributeMultiprocessorCount, f.device);
+        // a far update of a few tiles per compute unit leaves 32 units to the
+        // diagonal blocks and panels beside it (measured best at 4096); a
+        // larger one is the longer of the two streams and takes every unit
+        const int grid = nfar > 4 * units ? nfar : std::max(1, std::min(nfar, units - 32));
+        hipLaunchKernelGGL(k_update128, dim3(grid), dim3(NT), 0, f.aux, a, g0, g1, g2, nfar);
+      }
       update(UpdRange{g2, g2, g2, nbmax, g0, g1, g0}, f.aux);
       he = hipEventRecord(f.ev_far, f.aux);
       if (he != hipSuccess) return hip_fail(he, "hipEventRecord");
