@@ -533,13 +533,19 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   const int gi0 = I * TB, gj0 = J * TB;
   const T* X = (const T*)a.X;
 
-  // every global load of the prologue is issued before any is used
-  double lv[16], uv[16], ga[16], gb[16];
+  // every global load of the prologue is issued before any is used, in the
+  // order they are needed: the factor blocks, the operands of the two
+  // neighbour products, then X and the accumulated feedback
+  double lv[16], uv[16], ga[16], gb[16], gc[16], gd[16];
   load_blk(a.L + (int64_t)gi0 * a.mp + gi0, a.mp, lv);
   load_blk(a.U + (int64_t)gj0 * a.np + gj0, a.np, uv);
   if (I >= 1) {
     load_blk(a.L + (int64_t)gi0 * a.mp + (gi0 - TB), a.mp, ga);
     load_blk(a.E + (int64_t)(gi0 - TB) * a.np + gj0, a.np, gb);
+  }
+  if (J >= 1) {
+    load_blk(a.C + (int64_t)gi0 * a.np + (gj0 - TB), a.np, gc);
+    load_blk(a.U + (int64_t)(gj0 - TB) * a.np + gj0, a.np, gd);
   }
   double Dn[4][2][2], Rt[4][2][2], dl[2], du[4][2];
 #pragma unroll
@@ -583,15 +589,6 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
       for (int i = 0; i < 2; ++i) pv[c][i] = double2{0.0, 0.0};
   }
 #pragma unroll
-  for (int c = 0; c < 4; ++c)
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      Rt[c][i][0] += rv[c][i].x;
-      Rt[c][i][1] += rv[c][i].y;
-      Dn[c][i][0] = pv[c][i].x;
-      Dn[c][i][1] = pv[c][i].y;
-    }
-#pragma unroll
   for (int s = 0; s < 16; ++s) {
     const int e = t + NT * s, r = e >> 6, x = e & 63;
     sm.Ls[r][x] = lv[s];
@@ -604,20 +601,23 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   }
   if (t < 4) sm.done[t] = 0;
 
-  // feedback of the neighbouring tiles: L[I][I-1] E[I-1][J] and C[I][J-1] U[J-1][J]
+  // feedback of the neighbouring tiles: L[I][I-1] E[I-1][J] and C[I][J-1]
+  // U[J-1][J]; the accumulated feedback (P, R) is added first, as before
+  // either product
   Acc acc;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      Dn[c][i][0] = pv[c][i].x;
+      Dn[c][i][1] = pv[c][i].y;
+    }
   if (I >= 1) {
     acc.zero();
     put_a(sm.x.g, ga);
     put_b(sm.x.g, gb);
     __syncthreads();
     mma_blk(acc, sm.x.g);
-  }
-  if (J >= 1) {  // operands of the right product, in flight during the above
-    load_blk(a.C + (int64_t)gi0 * a.np + (gj0 - TB), a.np, ga);
-    load_blk(a.U + (int64_t)(gj0 - TB) * a.np + gj0, a.np, gb);
-  }
-  if (I >= 1) {
     __syncthreads();
     acc_to_lds<TB + 1>(acc, sm.x.T);
     __syncthreads();
@@ -628,11 +628,18 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) Dn[c][i][j] += sm.x.T[br + i][SS * c + 2 * q + j];
   }
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      Rt[c][i][0] += rv[c][i].x;
+      Rt[c][i][1] += rv[c][i].y;
+    }
   if (J >= 1) {
     acc.zero();
     __syncthreads();
-    put_a(sm.x.g, ga);
-    put_b(sm.x.g, gb);
+    put_a(sm.x.g, gc);
+    put_b(sm.x.g, gd);
     __syncthreads();
     mma_blk(acc, sm.x.g);
     __syncthreads();
