@@ -878,12 +878,13 @@ void schedule_tasks(int MT, int NTt, int g, std::vector<int4>& all, std::vector<
 // beside the sweeps; the others only when a sweep is done, so they start
 // loaded with its duration (and stay empty when the work fits beside the
 // sweeps).
+// (least-squares fit of measured bin durations at 4096 and 8192)
 constexpr double kSweepCost = 45.0;   // one tile sweep
-constexpr double kChunk4 = 5.0;       // 32-deep chunk onto 2 x 2 tiles
-constexpr double kChunk2 = 3.0;       // onto 2 x 1 or 1 x 2 tiles
-constexpr double kChunk1 = 1.8;       // onto one tile
+constexpr double kChunk4 = 5.1;       // 32-deep chunk onto 2 x 2 tiles
+constexpr double kChunk2 = 2.4;       // onto 2 x 1 or 1 x 2 tiles
+constexpr double kChunk1 = 1.2;       // onto one tile
 constexpr double kStartOw = 1.0;      // a delivery that overwrites
-constexpr double kStartAdd = 3.0;     // a delivery that adds to the old values
+constexpr double kStartAdd = 6.0;     // a delivery that adds to the old values
 gptq2d_status pack_bins(int MT, int NTt, int units, std::vector<int4>& all,
                         const std::vector<int>& off, std::vector<int4>& bins, std::vector<int>& boff) {
   const int S = MT + NTt - 1;
