@@ -228,6 +228,40 @@ __device__ __forceinline__ void put_bt(Stage64& st, const double r[16]) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Tile-contiguous storage of the factors and the sweep's matrices. A padded
+// matrix with TC tile columns is stored tile by tile: tile (I, J) occupies the
+// 4096 doubles from (I TC + J) 4096 on, in one of two orders:
+//   R (row-major tile): entry (r, c) at r 64 + c           (U, E, P, R)
+//   S (split tile): the two 64 x 32 column halves one after the other, each
+//     row-major: entry (r, c) at (c / 32) 2048 + r 32 + c % 32   (L, C)
+// L and C are the left operands of the deferred-feedback products, read in
+// 32-deep chunks: in S order four rows of a chunk are 1 KB of contiguous
+// memory, and in either order a chunk of a tile is 16 KB of it.
+// ---------------------------------------------------------------------------
+__host__ __device__ __forceinline__ int64_t tile_off(int I, int J, int TC) {
+  return ((int64_t)I * TC + J) << 12;
+}
+__host__ __device__ __forceinline__ int r_idx(int r, int c) { return (r << 6) + c; }
+__host__ __device__ __forceinline__ int s_idx(int r, int c) { return ((c >> 5) << 11) + (r << 5) + (c & 31); }
+// entry (i, j) of a matrix with TC tile columns
+__host__ __device__ __forceinline__ int64_t r_at(int64_t i, int64_t j, int TC) {
+  return tile_off((int)(i >> 6), (int)(j >> 6), TC) + r_idx((int)(i & 63), (int)(j & 63));
+}
+__host__ __device__ __forceinline__ int64_t s_at(int64_t i, int64_t j, int TC) {
+  return tile_off((int)(i >> 6), (int)(j >> 6), TC) + s_idx((int)(i & 63), (int)(j & 63));
+}
+
+// 64 x 64 tile in S order into registers, in load_blk's element order.
+__device__ __forceinline__ void load_blk_s(const double* p, double r[16]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    const int e = t + NT * s;
+    r[s] = p[s_idx(e >> 6, e & 63)];
+  }
+}
+
 // Device-scope error flags (bit set with a relaxed atomic OR).
 enum : int { FLAG_SINGULAR = 1, FLAG_NONFINITE = 2, FLAG_OVERFLOW = 4, FLAG_TIMEOUT = 8 };
 

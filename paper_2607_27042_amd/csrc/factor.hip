@@ -458,13 +458,20 @@ __device__ void chol_inv16(double* A, int lda, double* W, int ldw, int* flags) {
   }
 }
 
-__global__ __launch_bounds__(NT) void k_diag(FacArgs f, int kb) {
-  const Side& sd = f.s[blockIdx.x];
-  if (kb >= sd.nb) return;
-  constexpr int LD = TB + 1;
-  __shared__ double Am[TB][LD];      // the block, becomes Lc (lower)
-  __shared__ double Wm[TB][LD];      // Lc^{-1} (lower)
-  __shared__ double Tm[4][DS][DS + 1];
+constexpr int DLD = TB + 1;
+struct DiagSmem {
+  double Am[TB][DLD];      // the block, becomes Lc (lower)
+  double Wm[TB][DLD];      // Lc^{-1} (lower)
+  double Tm[4][DS][DS + 1];
+};
+
+// Diagonal block kb of one side by one work group: Cholesky factor in place
+// (gr) and its inverse into dinv.
+__device__ void diag_tile(const Side& sd, int kb, int* flags, DiagSmem& ds) {
+  constexpr int LD = DLD;
+  double(*Am)[LD] = ds.Am;
+  double(*Wm)[LD] = ds.Wm;
+  double(*Tm)[DS][DS + 1] = ds.Tm;
   const int t = threadIdx.x, w = t >> 6;
   double* blk = sd.gr + (int64_t)kb * TB * sd.dp + (int64_t)kb * TB;
   {
@@ -484,7 +491,7 @@ __global__ __launch_bounds__(NT) void k_diag(FacArgs f, int kb) {
   __syncthreads();
   for (int k = 0; k < 4; ++k) {
     const int o = DS * k;
-    if (w == k) chol_inv16(&Am[o][o], LD, &Wm[o][o], LD, f.flags);
+    if (w == k) chol_inv16(&Am[o][o], LD, &Wm[o][o], LD, flags);
     __syncthreads();
     if (w > k) {  // panel: L_wk = A_wk W_kk^T
       d4 acc = {0.0, 0.0, 0.0, 0.0};
@@ -524,6 +531,13 @@ __global__ __launch_bounds__(NT) void k_diag(FacArgs f, int kb) {
     blk[(int64_t)r * sd.dp + c] = Am[r][c];
     dv[e] = Wm[r][c];
   }
+}
+
+__global__ __launch_bounds__(NT) void k_diag(FacArgs f, int kb) {
+  __shared__ DiagSmem ds;
+  const Side& sd = f.s[blockIdx.x];
+  if (kb >= sd.nb) return;
+  diag_tile(sd, kb, f.flags, ds);
 }
 
 // ---------------------------------------------------------------------------
@@ -579,6 +593,8 @@ __global__ __launch_bounds__(NT) void k_panel(FacArgs f, int kb) {
 struct UpdRange {
   int qa, qb, sa, sb, k0, k1;
   int j0;  // S columns from j0 on (jb in [j0, k1))
+  int dg;  // the diagonal block whose update completes here (qa), factored
+           // by the same work group right after it; -1: none
 };
 
 __device__ __forceinline__ void upd_counts(const Side& sd, const UpdRange& r, int& nq, int& ns) {
@@ -611,7 +627,11 @@ __device__ void gemm_blocks(Acc& acc, const double* pa, int64_t lda, int64_t sa_
 }
 
 __global__ __launch_bounds__(NT) void k_update(FacArgs f, UpdRange r) {
-  __shared__ Stage64 st[2];
+  __shared__ union {
+    Stage64 st[2];
+    DiagSmem d;
+  } sm;
+  Stage64* st = sm.st;
   int b = blockIdx.x;
   int nq0, ns0;
   upd_counts(f.s[0], r, nq0, ns0);
@@ -647,6 +667,13 @@ __global__ __launch_bounds__(NT) void k_update(FacArgs f, UpdRange r) {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           out[(int64_t)acc_row(u, q) * sd.dp + acc_col(v)] = old[u][v][q] - acc.t[2 * u + v][q];
+    if (bi == r.dg && bj == r.dg) {
+      // no other work group of this launch reads this block (their operands
+      // are columns before k1 <= dg); its factorisation starts as soon as it
+      // is complete (written above, read back by the same work group)
+      __syncthreads();
+      diag_tile(sd, r.dg, f.flags, sm.d);
+    }
   } else {
     b -= nq;
     const int ib = r.sa + b / (k1 - r.j0), jb = r.j0 + b % (k1 - r.j0);
@@ -829,6 +856,8 @@ __global__ __launch_bounds__(NT) void k_update128(FacArgs f, int g0, int g1, int
 //   side 0: L[i][j] = Li[d-1-j][d-1-i] Lc[d-1-j][d-1-j]  (i > j), lower tiles
 //   side 1: U[i][j] = Li[d-1-i][d-1-j] Lc[d-1-i][d-1-i]  (j > i), upper tiles
 //   1/Lambda[i] = Lc[d-1-i][d-1-i]^2; the padding becomes an identity block.
+// L is stored tile by tile in S order, U in R order (device.hpp); only the
+// triangle's tiles are written, and only they are ever read.
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(NT) void k_finalize(FacArgs f) {
@@ -863,7 +892,7 @@ __global__ __launch_bounds__(NT) void k_finalize(FacArgs f) {
     } else {
       val = (j > i) ? S[63 - a][63 - b] * sc[63 - a] : 0.0;
     }
-    sd.out[(int64_t)i * dp + j] = val;
+    sd.out[side == 0 ? s_at(i, j, sd.nb) : r_at(i, j, sd.nb)] = val;
   }
   if (bi == bj && t < TB) {
     const int i = bi * TB + t;
@@ -876,13 +905,15 @@ __global__ void k_zero_int(int* p, int n) {
   if (i < n) p[i] = 0;
 }
 
-// factor export: dense triangle out of the padded storage, lam = 1 / dl.
+// factor export: dense triangle out of the tiled storage (L in S order, U in
+// R order), lam = 1 / dl.
 __global__ void k_export_tri(const double* src, int dp, int d, double* dst, int64_t ld, int lower) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= (int64_t)d * d) return;
   const int i = (int)(e / d), j = (int)(e % d);
   const bool keep = lower ? (j <= i) : (j >= i);
-  dst[(int64_t)i * ld + j] = keep ? (i == j ? 1.0 : src[(int64_t)i * dp + j]) : 0.0;
+  const int64_t at = lower ? s_at(i, j, dp / TB) : r_at(i, j, dp / TB);
+  dst[(int64_t)i * ld + j] = keep ? (i == j ? 1.0 : src[at]) : 0.0;
 }
 
 __global__ void k_export_lam(const double* dl, int d, double* lam) {
@@ -899,7 +930,7 @@ __global__ void k_import_tri(const double* src, int64_t ld, int d, int dp, doubl
   else if (i >= d || j >= d) v = 0.0;
   else if (lower ? (j < i) : (j > i)) v = src[(int64_t)i * ld + j];
   else v = 0.0;
-  dst[e] = v;
+  dst[lower ? s_at(i, j, dp / TB) : r_at(i, j, dp / TB)] = v;
 }
 
 __global__ void k_import_lam(const double* lam, int d, int dp, double* dl) {
@@ -1003,17 +1034,20 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
   for (int g0 = 0; g0 < nbmax; g0 += GROUP) {
     const int g1 = std::min(g0 + GROUP, nbmax), g2 = std::min(g1 + GROUP, nbmax);
     for (int kb = g0; kb < g1; ++kb) {
-      hipLaunchKernelGGL(k_diag, dim3(2), dim3(NT), 0, s, a, kb);
+      // the diagonal block of every later panel is factored by the update
+      // that completes it (the in-group update of the panel before, or the
+      // group's near update for the next group's first panel)
+      if (kb == 0) hipLaunchKernelGGL(k_diag, dim3(2), dim3(NT), 0, s, a, kb);
       const int np_ = h_panel_count(nb0, kb) + h_panel_count(nb1, kb);
       if (np_ > 0) hipLaunchKernelGGL(k_panel, dim3(np_), dim3(NT), 0, s, a, kb);
-      if (kb + 1 < g1) update(UpdRange{kb + 1, g1, kb + 1, g1, kb, kb + 1, 0}, s);
+      if (kb + 1 < g1) update(UpdRange{kb + 1, g1, kb + 1, g1, kb, kb + 1, 0, kb + 1}, s);
     }
     if (far_pending) {
       he = hipStreamWaitEvent(s, f.ev_far, 0);
       if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
       far_pending = false;
     }
-    update(UpdRange{g1, g2, g1, g2, g0, g1, 0}, s);
+    update(UpdRange{g1, g2, g1, g2, g0, g1, 0, g1}, s);
     if (g2 < nbmax) {
       he = hipEventRecord(f.ev_near, s);
       if (he == hipSuccess) he = hipStreamWaitEvent(f.aux, f.ev_near, 0);
@@ -1033,7 +1067,7 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
         const int grid = nfar > 4 * units ? nfar : std::max(1, std::min(nfar, units - 32));
         hipLaunchKernelGGL(k_update128, dim3(grid), dim3(NT), 0, f.aux, a, g0, g1, g2, nfar);
       }
-      update(UpdRange{g2, g2, g2, nbmax, g0, g1, g0}, f.aux);
+      update(UpdRange{g2, g2, g2, nbmax, g0, g1, g0, -1}, f.aux);
       he = hipEventRecord(f.ev_far, f.aux);
       if (he != hipSuccess) return hip_fail(he, "hipEventRecord");
       far_pending = true;

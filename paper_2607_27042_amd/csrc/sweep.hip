@@ -87,7 +87,8 @@ struct SweepSmem {
 // 16-byte pieces permuted by an XOR with the row's position in the block and
 // every block padded by 64 bytes (an MFMA operand read of 16 rows then hits 16
 // distinct bank groups), the right operand as rows b[k][col] padded to 130
-// doubles. Every load instruction reads whole 256-byte row segments.
+// doubles. With the tile-contiguous storage a left-operand load reads 1 KB of
+// contiguous memory and a right-operand load two 512-byte runs.
 constexpr int KQ = 32;
 constexpr int AQ = 4 * KQ + 8;  // doubles per 4-row block of the left operand (64 B pad)
 struct TaskChunk {
@@ -113,12 +114,16 @@ __device__ __forceinline__ double load_x(const T* X, int64_t ldx, int gi, int gj
 }
 
 // Operands of one delivery (uniform over the work group): out (+)= A B with
-// A the (64 nr) x (64 K) source panel and B the (64 K) x (64 nc) panel.
+// A the (64 nr) x (64 K) source panel and B the (64 K) x (64 nc) panel, all
+// tile-contiguous: A points at its first tile (S order), the next tile row
+// ars doubles on and the next source tile 4096 on; B at its first tile (R
+// order), the next source tile row bks on and the next tile column 4096 on;
+// out at the first target tile (R order), the next tile row ors on.
 struct TaskOp {
   const double* A;
   const double* B;
   double* out;
-  int64_t lda;
+  int64_t ars, bks, ors;
   int nch, ow, nr, nc;
 };
 
@@ -130,16 +135,18 @@ __device__ __forceinline__ TaskOp task_op(const StageArgs& a, int4 tk) {
   T.nr = ((tk.x >> 2) & 1) + 1;
   T.nc = ((tk.x >> 3) & 1) + 1;
   T.nch = (s1 - s0) * (TB / KQ);
+  T.bks = tile_off(1, 0, a.NT);
+  T.ors = tile_off(1, 0, a.NT);
   if (dir == 0) {
-    T.A = a.L + (int64_t)ti * TB * a.mp + (int64_t)s0 * TB;
-    T.lda = a.mp;
-    T.B = a.E + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
-    T.out = a.P + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
+    T.A = a.L + tile_off(ti, s0, a.MT);
+    T.ars = tile_off(1, 0, a.MT);
+    T.B = a.E + tile_off(s0, tj, a.NT);
+    T.out = a.P + tile_off(ti, tj, a.NT);
   } else {
-    T.A = a.C + (int64_t)ti * TB * a.np + (int64_t)s0 * TB;
-    T.lda = a.np;
-    T.B = a.U + (int64_t)s0 * TB * a.np + (int64_t)tj * TB;
-    T.out = a.R + (int64_t)ti * TB * a.np + (int64_t)tj * TB;
+    T.A = a.C + tile_off(ti, s0, a.NT);
+    T.ars = tile_off(1, 0, a.NT);
+    T.B = a.U + tile_off(s0, tj, a.NT);
+    T.out = a.R + tile_off(ti, tj, a.NT);
   }
   return T;
 }
@@ -150,25 +157,26 @@ typedef __attribute__((address_space(3))) void lds_void;
 // 4 nr left-operand row blocks.
 __device__ __forceinline__ int task_loads(const TaskOp& T) { return 8 + 4 * T.nr; }
 
-// Chunk c of task T into d: wave w moves the left-operand row blocks
-// j = w + 4i (rows 4j .. 4j+3, i < 4 nr) and the right-operand rows k = w + 4i
-// (i < 8), each a 1 KB direct global -> LDS load. Lane l of a left-operand
-// load takes the 16-byte piece (l & 15) ^ (l >> 4) of row 4j + (l >> 4); of a
-// right-operand load the columns 2l, 2l+1 (clamped to the target: never used
-// past it).
-__device__ __forceinline__ void task_issue(const TaskOp& T, int c, TaskChunk& d, int w, int l,
-                                           int64_t ldb) {
+// Chunk c of task T into d (source tile c / 2, its columns (rows of B)
+// 32 (c % 2) ..): wave w moves the left-operand row blocks j = w + 4i (rows
+// 4j .. 4j+3, i < 4 nr: 1 KB of contiguous memory in S order) and the
+// right-operand rows k = w + 4i (i < 8), each a 1 KB direct global -> LDS
+// load. Lane l of a left-operand load takes the 16-byte piece
+// (l & 15) ^ (l >> 4) of row 4j + (l >> 4); of a right-operand load the
+// columns 2l, 2l+1 (clamped to the target: never used past it).
+__device__ __forceinline__ void task_issue(const TaskOp& T, int c, TaskChunk& d, int w, int l) {
   const int ar = l >> 4, ap = (l & 15) ^ ar;
-  const int64_t k0 = (int64_t)c * KQ;
-  const double* pb = T.B + min(2 * l, TB * T.nc - 2) + k0 * ldb;
+  const double* ac = T.A + (int64_t)(c >> 1) * 4096 + (c & 1) * 2048;
+  const int col = min(2 * l, TB * T.nc - 2);
+  const double* pb = T.B + (int64_t)(c >> 1) * T.bks + (c & 1) * 32 * TB + (col >> 6) * 4096 + (col & 63);
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const int j = w + 4 * i;
     if (i < 4 * T.nr) {
-      const double* pa = T.A + (int64_t)(4 * j + ar) * T.lda + 2 * ap + k0;
+      const double* pa = ac + (j >> 4) * T.ars + (4 * (j & 15) + ar) * 32 + 2 * ap;
       __builtin_amdgcn_global_load_lds((const void*)pa, (lds_void*)&d.a[j][0], 16, 0, 0);
     }
-    __builtin_amdgcn_global_load_lds((const void*)(pb + j * ldb), (lds_void*)&d.b[j][0], 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)(pb + j * TB), (lds_void*)&d.b[j][0], 16, 0, 0);
   }
 }
 
@@ -187,17 +195,22 @@ __device__ __forceinline__ void task_part(const TaskOp& T, int w, int& rb, int& 
 
 // Accumulators of the wave's part: the old target values (a delivery that
 // adds) or zero (one that overwrites).
+// Entry (row, col) of a target (rows and columns counted from its first
+// tile) relative to T.out.
+__device__ __forceinline__ int64_t task_at(const TaskOp& T, int row, int col) {
+  return (row >> 6) * T.ors + (col >> 6) * 4096 + r_idx(row & 63, col & 63);
+}
+
 template <int NI, int NJ>
-__device__ __forceinline__ void task_init(d4 (&acc)[4][4], const TaskOp& T, int rb, int cb, int l,
-                                          int64_t np) {
+__device__ __forceinline__ void task_init(d4 (&acc)[4][4], const TaskOp& T, int rb, int cb, int l) {
   if (!T.ow) {
-    const double* o = T.out + (int64_t)(rb + (l >> 4)) * np + cb + (l & 15);
 #pragma unroll
     for (int i = 0; i < NI; ++i)
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[i][j][r] = o[(int64_t)(16 * i + 4 * r) * np + 16 * j];
+        for (int r = 0; r < 4; ++r)
+          acc[i][j][r] = T.out[task_at(T, rb + 16 * i + 4 * r + (l >> 4), cb + 16 * j + (l & 15))];
     // the accumulators are complete before the chunk loop (so that no wait
     // for them lands inside it, where it would also wait for the next chunk)
     __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
@@ -211,14 +224,14 @@ __device__ __forceinline__ void task_init(d4 (&acc)[4][4], const TaskOp& T, int 
 
 template <int NI, int NJ>
 __device__ __forceinline__ void task_store(const d4 (&acc)[4][4], const TaskOp& T, int rb, int cb,
-                                           int l, int64_t np) {
-  double* o = T.out + (int64_t)(rb + (l >> 4)) * np + cb + (l & 15);
+                                           int l) {
 #pragma unroll
   for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int j = 0; j < NJ; ++j)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * np + 16 * j] = acc[i][j][r];
+      for (int r = 0; r < 4; ++r)
+        T.out[task_at(T, rb + 16 * i + 4 * r + (l >> 4), cb + 16 * j + (l & 15))] = acc[i][j][r];
 }
 
 // One staged chunk on MFMA: acc[i][j] += A(rows rb + 16 i ..) B(cols cb + 16 j ..).
@@ -268,22 +281,21 @@ __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& 
   constexpr int NR = NI == 4 && NJ == 4 ? 2 : NI == 2 && NJ == 4 ? 2 : 1;  // target rows in tiles
   constexpr int NL = 8 + 4 * NR;  // load instructions per wave and chunk
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
-  const int64_t np = a.np;
   d4 acc[4][4];
   TaskOp T = task_op(a, tk[0]);
   TaskOp Tn = T;
   int rb, cb;
   task_part(T, w, rb, cb);
-  task_issue(T, 0, sm.buf[0], w, l, np);
-  task_init<NI, NJ>(acc, T, rb, cb, l, np);
+  task_issue(T, 0, sm.buf[0], w, l);
+  task_init<NI, NJ>(acc, T, rb, cb, l);
   int idx = 0, c = 0, p = 0;
   for (;;) {
     const bool last = c + 1 == T.nch;
     if (!last) {
-      task_issue(T, c + 1, sm.buf[p ^ 1], w, l, np);
+      task_issue(T, c + 1, sm.buf[p ^ 1], w, l);
     } else if (idx + 1 < n) {
       Tn = task_op(a, tk[idx + 1]);
-      task_issue(Tn, 0, sm.buf[p ^ 1], w, l, np);
+      task_issue(Tn, 0, sm.buf[p ^ 1], w, l);
     }
     // chunk c has landed
     if (!last || idx + 1 < n) {
@@ -301,11 +313,11 @@ __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& 
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     p ^= 1;
     if (last) {
-      task_store<NI, NJ>(acc, T, rb, cb, l, np);
+      task_store<NI, NJ>(acc, T, rb, cb, l);
       if (++idx == n) break;
       T = Tn;
       c = 0;
-      task_init<NI, NJ>(acc, T, rb, cb, l, np);
+      task_init<NI, NJ>(acc, T, rb, cb, l);
     } else {
       ++c;
     }
@@ -370,6 +382,8 @@ __device__ __forceinline__ void mma16k(d4& acc, const double* pa, int lda, const
 // Per-lane constants of a band sweep.
 struct Band {
   int w, l, p, q, br, gi0, gj0;
+  double* Et;      // the tile's E (R order) and C (S order)
+  double* Ct;
   double l10;      // L[br+1][br]
   double dl[2];    // 1 / lamL of the lane's two rows
 };
@@ -498,8 +512,8 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
     double ev[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) ev[j] = rint(yf[i][j]) - yf[i][j];
-    *reinterpret_cast<double2*>(a.E + (int64_t)gi * a.np + gj) = double2{ev[0], ev[1]};
-    *reinterpret_cast<double2*>(a.C + (int64_t)gi * a.np + gj) = double2{cf[i][0], cf[i][1]};
+    *reinterpret_cast<double2*>(b.Et + r_idx(br + i, uc + 2 * q)) = double2{ev[0], ev[1]};
+    *reinterpret_cast<double2*>(b.Ct + s_idx(br + i, uc + 2 * q)) = double2{cf[i][0], cf[i][1]};
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const double yv = yf[i][j];
@@ -537,15 +551,15 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   // order they are needed: the factor blocks, the operands of the two
   // neighbour products, then X and the accumulated feedback
   double lv[16], uv[16], ga[16], gb[16], gc[16], gd[16];
-  load_blk(a.L + (int64_t)gi0 * a.mp + gi0, a.mp, lv);
-  load_blk(a.U + (int64_t)gj0 * a.np + gj0, a.np, uv);
+  load_blk_s(a.L + tile_off(I, I, a.MT), lv);
+  load_blk(a.U + tile_off(J, J, a.NT), TB, uv);
   if (I >= 1) {
-    load_blk(a.L + (int64_t)gi0 * a.mp + (gi0 - TB), a.mp, ga);
-    load_blk(a.E + (int64_t)(gi0 - TB) * a.np + gj0, a.np, gb);
+    load_blk_s(a.L + tile_off(I, I - 1, a.MT), ga);
+    load_blk(a.E + tile_off(I - 1, J, a.NT), TB, gb);
   }
   if (J >= 1) {
-    load_blk(a.C + (int64_t)gi0 * a.np + (gj0 - TB), a.np, gc);
-    load_blk(a.U + (int64_t)(gj0 - TB) * a.np + gj0, a.np, gd);
+    load_blk_s(a.C + tile_off(I, J - 1, a.NT), gc);
+    load_blk(a.U + tile_off(J - 1, J, a.NT), TB, gd);
   }
   double Dn[4][2][2], Rt[4][2][2], dl[2], du[4][2];
 #pragma unroll
@@ -569,7 +583,7 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
     for (int c = 0; c < 4; ++c)
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        rv[c][i] = *reinterpret_cast<const double2*>(a.R + (int64_t)(gi0 + br + i) * a.np + gj0 + SS * c + 2 * q);
+        rv[c][i] = *reinterpret_cast<const double2*>(a.R + tile_off(I, J, a.NT) + r_idx(br + i, SS * c + 2 * q));
   } else {
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -581,7 +595,7 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
     for (int c = 0; c < 4; ++c)
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        pv[c][i] = *reinterpret_cast<const double2*>(a.P + (int64_t)(gi0 + br + i) * a.np + gj0 + SS * c + 2 * q);
+        pv[c][i] = *reinterpret_cast<const double2*>(a.P + tile_off(I, J, a.NT) + r_idx(br + i, SS * c + 2 * q));
   } else {
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -663,6 +677,8 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
   }
   Band bd;
   bd.w = w; bd.l = l; bd.p = p; bd.q = q; bd.br = br; bd.gi0 = gi0; bd.gj0 = gj0;
+  bd.Et = a.E + tile_off(I, J, a.NT);
+  bd.Ct = a.C + tile_off(I, J, a.NT);
   bd.l10 = sm.Ls[br + 1][br];
   bd.dl[0] = dl[0];
   bd.dl[1] = dl[1];
