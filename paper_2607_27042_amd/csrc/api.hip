@@ -106,6 +106,11 @@ gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
   A(&f->gram[1], np * np);
   A(&f->inv[1], np * np);
   A(&f->dinv[1], np * TB);
+  if (hipDeviceGetAttribute(&f->cus, hipDeviceAttributeMultiprocessorCount, f->device) != hipSuccess ||
+      f->cus <= 0)
+    f->cus = 256;
+  const size_t gpd = gram_part_doubles(f->m, f->n, f->cus);
+  if (gpd > 0) A(&f->gpart, gpd);
   if (st == GPTQ2D_OK) {
     st = alloc(f, &p, 256);
     if (st == GPTQ2D_OK) {

@@ -235,44 +235,51 @@ __device__ __forceinline__ void gram_issue(const double* Sp, const double* Sq, i
   }
 }
 
-__global__ __launch_bounds__(NT) void k_gram128(FacArgs f, int sides) {
-  __shared__ GramChunk buf[2];
-  const int nt0 = f.s[0].d / 128;
-  const int t0 = (sides & 1) ? nt0 * (nt0 + 1) / 2 : 0;
-  // work groups are dealt round-robin to the eight L2 domains (XCDs): give
-  // each domain a contiguous run of tiles, so that the tiles it runs at the
-  // same time share their row panel (tri_index enumerates row by row)
-  // (domain x holds the blocks b = x mod 8, q of them, and gets the tiles
-  // from x q + min(x, r) on, with q, r the quotient and remainder by 8)
-  const int ntile = gridDim.x, q8 = ntile / 8, r8 = ntile % 8;
-  const int x = blockIdx.x % 8;
-  int b = x * q8 + min(x, r8) + (int)blockIdx.x / 8;
-  const int side = b < t0 ? 0 : 1;
-  if (side == 1) b -= t0;
-  const Side& sd = f.s[side];
-  int bp, bq;
-  tri_index(b, bp, bq);
+// The 32-deep chunks of all 128 x 128 Gram tiles, tile by tile (side 0's
+// tiles first), form one sequence of work units, dealt out as G contiguous
+// ranges of nearly equal length, one per work group, so that no round of
+// work groups runs with most of the device idle. A range is at least one
+// tile long: a tile is either inside one range (stored directly) or split
+// between two neighbouring ranges, whose partial products go to a pair of
+// scratch slots (one per range boundary) and are added by k_gram_fix in a
+// fixed order.
+struct GramPlan {
+  int t0, t1;          // tiles of side 0 and side 1 on this path
+  int nch0, nch1;      // chunks per tile on each side
+  int64_t units;       // t0 nch0 + t1 nch1
+  int G;               // work groups (ranges)
+  __host__ __device__ int64_t lo(int j) const { return units * j / G; }
+  // unit u -> side, tile, first chunk
+  __host__ __device__ void at(int64_t u, int& side, int& b, int& c) const {
+    const int64_t u0 = (int64_t)t0 * nch0;
+    if (u < u0) { side = 0; b = (int)(u / nch0); c = (int)(u % nch0); }
+    else { side = 1; b = (int)((u - u0) / nch1); c = (int)((u - u0) % nch1); }
+  }
+};
+
+// Chunks c0 .. c1-1 of the tile (bp, bq) of one side into acc (zeroed here).
+__device__ __forceinline__ void gram_part(const Side& sd, int bp, int bq, int c0, int c1, GramChunk* buf,
+                                          d4 (&acc)[4][4]) {
   const int d = sd.d;
   const double* Sp = sd.li + (int64_t)(128 * bp) * d;
   const double* Sq = sd.li + (int64_t)(128 * bq) * d;
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   const int qr = w >> 1, qc = w & 1, r0 = l & 15;
-  d4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
-  const int nch = d / GQ;
-  gram_issue(Sp, Sq, d, 0, buf[0], w, l);
-  for (int c = 0; c < nch; ++c) {
-    if (c + 1 < nch) {
-      gram_issue(Sp, Sq, d, c + 1, buf[(c + 1) & 1], w, l);
+  gram_issue(Sp, Sq, d, c0, buf[0], w, l);
+  for (int c = c0; c < c1; ++c) {
+    const int cb = (c - c0) & 1;
+    if (c + 1 < c1) {
+      gram_issue(Sp, Sq, d, c + 1, buf[cb ^ 1], w, l);
       __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16): chunk c has landed
     } else {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
     asm volatile("s_barrier" ::: "memory");  // the wait above covers this wave's part
-    const GramChunk& st = buf[c & 1];
+    const GramChunk& st = buf[cb];
     // operands of k-step kk + 1 are read while kk is on MFMA (two register
     // sets), the reads spread between the MFMAs
     double av[2][4], bv[2][4];
@@ -307,7 +314,13 @@ __global__ __launch_bounds__(NT) void k_gram128(FacArgs f, int sides) {
     }
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // buffer refilled next
   }
-  if (bp == bq && qr < qc) return;  // upper quadrant of a diagonal tile
+}
+
+// The wave's 64 x 64 quadrant of a finished tile into the Gram (the upper
+// quadrant of a diagonal tile is not kept).
+__device__ __forceinline__ void gram_store(const Side& sd, int bp, int bq, const d4 (&acc)[4][4]) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, qr = w >> 1, qc = w & 1;
+  if (bp == bq && qr < qc) return;
   double* o = sd.gr + (int64_t)(128 * bp + 64 * qr + (l >> 4)) * sd.dp + 128 * bq + 64 * qc + (l & 15);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -315,6 +328,95 @@ __global__ __launch_bounds__(NT) void k_gram128(FacArgs f, int sides) {
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * sd.dp + 16 * j] = acc[i][j][r];
+}
+
+// Scratch slot of a partial product: every thread keeps its 64 values in
+// the accumulator order, 256 threads side by side.
+__device__ __forceinline__ double* gram_slot(double* part, int slot, int h) {
+  return part + ((int64_t)(2 * slot + h) << 14) + threadIdx.x;
+}
+
+__global__ __launch_bounds__(NT) void k_gram128(FacArgs f, GramPlan pl, double* part) {
+  __shared__ GramChunk buf[2];
+  // work groups are dealt round-robin to the eight L2 domains (XCDs): give
+  // each domain a contiguous run of ranges, so that the tiles it runs at the
+  // same time share their row panel (tri_index enumerates row by row)
+  // (domain x holds the work groups i = x mod 8, q of them, and gets the
+  // ranges from x q + min(x, r) on, with q, r the quotient and remainder by 8)
+  const int q8 = pl.G / 8, r8 = pl.G % 8;
+  const int x = blockIdx.x % 8;
+  const int jr = x * q8 + min(x, r8) + (int)blockIdx.x / 8;
+  const int64_t hi = pl.lo(jr + 1);
+  d4 acc[4][4];
+  for (int64_t u = pl.lo(jr); u < hi;) {
+    int side, b, c0;
+    pl.at(u, side, b, c0);
+    const Side& sd = f.s[side];
+    const int nch = side == 0 ? pl.nch0 : pl.nch1;
+    const int c1 = (int)min((int64_t)nch, c0 + (hi - u));
+    int bp, bq;
+    tri_index(b, bp, bq);
+    if (u != pl.lo(jr)) __syncthreads();  // the staging buffers are reused
+    gram_part(sd, bp, bq, c0, c1, buf, acc);
+    if (c0 == 0 && c1 == nch) {
+      gram_store(sd, bp, bq, acc);
+    } else {
+      // the head of a tile ends this range (slot jr), the tail of one starts it (slot jr - 1)
+      double* o = c0 == 0 ? gram_slot(part, jr, 0) : gram_slot(part, jr - 1, 1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o[(int64_t)(((i * 4 + j) * 4 + r) * NT)] = acc[i][j][r];
+    }
+    u += c1 - c0;
+  }
+}
+
+// Tiles split between ranges jr and jr + 1: head + tail, stored as a finished tile.
+__global__ __launch_bounds__(NT) void k_gram_fix(FacArgs f, GramPlan pl, const double* part) {
+  const int jr = blockIdx.x;
+  const int64_t u = pl.lo(jr + 1);
+  int side, b, c;
+  pl.at(u, side, b, c);
+  if (c == 0) return;  // the boundary falls between tiles
+  const double* h0 = gram_slot(const_cast<double*>(part), jr, 0);
+  const double* h1 = gram_slot(const_cast<double*>(part), jr, 1);
+  d4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t e = (int64_t)(((i * 4 + j) * 4 + r) * NT);
+        acc[i][j][r] = h0[e] + h1[e];
+      }
+  int bp, bq;
+  tri_index(b, bp, bq);
+  gram_store(f.s[side], bp, bq, acc);
+}
+
+static GramPlan gram_plan(int m, int n, int fast, int cus) {
+  GramPlan pl;
+  const int n0 = m / 128, n1 = n / 128;
+  pl.t0 = (fast & 1) ? n0 * (n0 + 1) / 2 : 0;
+  pl.t1 = (fast & 2) ? n1 * (n1 + 1) / 2 : 0;
+  pl.nch0 = std::max(1, m / GQ);
+  pl.nch1 = std::max(1, n / GQ);
+  pl.units = (int64_t)pl.t0 * pl.nch0 + (int64_t)pl.t1 * pl.nch1;
+  const int64_t nmax = std::max(pl.t0 ? pl.nch0 : 1, pl.t1 ? pl.nch1 : 1);
+  // every range at least one tile long: a tile meets at most one boundary
+  pl.G = (int)std::max<int64_t>(1, std::min<int64_t>(std::max(cus, 1), pl.units / nmax));
+  return pl;
+}
+
+size_t gram_part_doubles(int m, int n, int cus) {
+  const int fast = (m % 128 == 0 ? 1 : 0) | (n % 128 == 0 ? 2 : 0);
+  if (!fast) return 0;
+  const GramPlan pl = gram_plan(m, n, fast, cus);
+  return pl.G > 1 ? (size_t)2 * pl.G * 16384 : 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -988,13 +1090,12 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
   // Gram: sides whose dimension is a multiple of 128 through the prepared
   // panel and 128 x 128 tiles, the others with 64 x 64 tiles straight from
   // the input
-  int fast = 0, slow = 0, nprep = 0, n128 = 0, nslow = 0;
+  int fast = 0, slow = 0, nprep = 0, nslow = 0;
   for (int sd = 0; sd < 2; ++sd) {
     const int d = a.s[sd].d, nb = a.s[sd].nb;
     if (d % 128 == 0) {
       fast |= 1 << sd;
       nprep += (d / TB) * (d / TB);
-      n128 += (d / 128) * (d / 128 + 1) / 2;
     } else {
       slow |= 1 << sd;
       nslow += nb * (nb + 1) / 2;
@@ -1007,7 +1108,9 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
     else
       hipLaunchKernelGGL(k_gram_prep<double>, dim3(nprep), dim3(NT), 0, s, a, (const double*)A,
                          lda, (const double*)B, ldb, fast);
-    hipLaunchKernelGGL(k_gram128, dim3(n128), dim3(NT), 0, s, a, fast);
+    const GramPlan pl = gram_plan(f.m, f.n, fast, f.cus);
+    hipLaunchKernelGGL(k_gram128, dim3(pl.G), dim3(NT), 0, s, a, pl, f.gpart);
+    if (pl.G > 1) hipLaunchKernelGGL(k_gram_fix, dim3(pl.G - 1), dim3(NT), 0, s, a, pl, (const double*)f.gpart);
   }
   if (slow) {
     if (dt == GPTQ2D_F32)

@@ -32,8 +32,8 @@ struct Factors {
   int MT = 0, NT = 0;   // tile counts
   int device = 0;
   // outputs of the factorisation (fp64, padded with an identity block)
-  double* L = nullptr;   // mp x mp, ld mp; unit lower; upper part not kept
-  double* U = nullptr;   // np x np, ld np; unit upper; lower part not kept
+  double* L = nullptr;   // mp x mp, tile by tile in S order; unit lower; upper tiles not kept
+  double* U = nullptr;   // np x np, tile by tile in R order; unit upper; lower tiles not kept
   double* dL = nullptr;  // mp: 1 / lamL
   double* dU = nullptr;  // np: 1 / lamU
   // factorisation scratch, one set per side
@@ -41,6 +41,8 @@ struct Factors {
   double* inv[2] = {nullptr, nullptr};   // inverse of that Cholesky factor
   double* dinv[2] = {nullptr, nullptr};  // inverses of its 64 x 64 diagonal blocks
   int* flags = nullptr;                  // device error bits of the factorisation
+  double* gpart = nullptr;               // partial Gram tiles split between work groups
+  int cus = 256;                         // compute units of the device
   // second stream of the factorisation: the far part of each group's
   // trailing update runs there, next to the following group's panels
   hipStream_t aux = nullptr;
@@ -72,6 +74,8 @@ void set_error(const std::string& msg);
 gptq2d_status hip_fail(hipError_t e, const char* what);
 
 // factorisation launches (enqueued on stream, no synchronisation)
+// doubles of scratch for the Gram tiles split between work groups
+size_t gram_part_doubles(int m, int n, int cus);
 gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t lda,
                             const void* B, int64_t ldb, hipStream_t s);
 gptq2d_status launch_export(const Factors& f, double* L, int64_t ldl, double* U, int64_t ldu,
