@@ -686,10 +686,10 @@ __global__ __launch_bounds__(NT) void k_panel(FacArgs f, int kb) {
 //   S[ib][jb] += sum_kb Lc[ib][kb] Li[kb][jb]        (sa <= ib < sb, jb < k1,
 //                                                      max(k0, jb) <= kb < k1)
 // S is the running sum of the triangular inverse, kept in place in Li; its
-// first contribution (kb = jb) overwrites. Called with one panel for the
-// columns / rows still inside the current group of panels, and with the
-// whole group for everything beyond it, so the bulk of the trailing work is
-// done with 256-deep products.
+// first contribution (kb = jb) overwrites. Called, before each panel of a
+// group, for that panel's column and row with the group's earlier panels,
+// and with the whole group for everything beyond it, so the bulk of the
+// trailing work is done with products as deep as the group.
 // ---------------------------------------------------------------------------
 
 struct UpdRange {
@@ -737,6 +737,12 @@ __global__ __launch_bounds__(NT) void k_update(FacArgs f, UpdRange r) {
   int b = blockIdx.x;
   int nq0, ns0;
   upd_counts(f.s[0], r, nq0, ns0);
+  // the two sides' diagonal blocks (the first Q tile of each side) go to
+  // the first two work groups: their factorisation is the longest chain
+  if (r.dg >= 0 && nq0 + ns0 > 1 && nq0 + ns0 < (int)gridDim.x) {
+    if (b == 1) b = nq0 + ns0;
+    else if (b == nq0 + ns0) b = 1;
+  }
   const bool s1 = b >= nq0 + ns0;
   const Side& sd = s1 ? f.s[1] : f.s[0];
   if (s1) b -= nq0 + ns0;
@@ -1124,14 +1130,17 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
     const int nu = h_upd_count(nb0, r) + h_upd_count(nb1, r);
     if (nu > 0) hipLaunchKernelGGL(k_update, dim3(nu), dim3(NT), 0, st, a, r);
   };
-  // Groups of four panels. Inside a group each panel updates only the
-  // group's remaining columns (and rows of the inverse sum); afterwards the
-  // whole group updates everything beyond it with 256-deep products: the
-  // next group's four columns on the caller's stream (they are needed
-  // first), the rest on the second stream, where it overlaps the next
-  // group's diagonal blocks and panels. Before touching tiles that the far
-  // part writes, the caller's stream waits for it.
-  constexpr int GROUP = 4;
+  // Groups of GROUP panels (an even count: the far part works on pairs of
+  // block columns). Inside a group, before each panel, its column of Q and
+  // row of S receive the group's earlier panels (left-looking, so that the
+  // critical chain has few work groups); afterwards the whole group updates
+  // everything beyond it with (64 GROUP)-deep products: the next group's
+  // columns on the caller's stream (they are needed first), the rest on the
+  // second stream, where it overlaps the next group's diagonal blocks and
+  // panels. Before touching tiles that the far part writes, the caller's
+  // stream waits for it. Eight panels per group from 96 block columns on
+  // (measured faster at 8192), four below (at 4096).
+  const int GROUP = nbmax > 96 ? 8 : 4;
   hipError_t he = hipSuccess;
   bool far_pending = false;
   for (int g0 = 0; g0 < nbmax; g0 += GROUP) {
@@ -1143,7 +1152,10 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
       if (kb == 0) hipLaunchKernelGGL(k_diag, dim3(2), dim3(NT), 0, s, a, kb);
       const int np_ = h_panel_count(nb0, kb) + h_panel_count(nb1, kb);
       if (np_ > 0) hipLaunchKernelGGL(k_panel, dim3(np_), dim3(NT), 0, s, a, kb);
-      if (kb + 1 < g1) update(UpdRange{kb + 1, g1, kb + 1, g1, kb, kb + 1, 0, kb + 1}, s);
+      // left-looking inside the group: the next panel's column of Q and row
+      // of S get all of the group's finished panels at once (the later
+      // columns wait for their own turn)
+      if (kb + 1 < g1) update(UpdRange{kb + 1, kb + 2, kb + 1, kb + 2, g0, kb + 1, 0, kb + 1}, s);
     }
     if (far_pending) {
       he = hipStreamWaitEvent(s, f.ev_far, 0);
