@@ -272,10 +272,12 @@ __device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, i
 }
 
 // A run of n deliveries of one target shape (NI x NJ blocks per wave),
-// streamed through one double-buffered pipeline: the first chunk of the next
-// delivery is loaded while the last chunk of the current one is on MFMA, so
-// deliveries follow each other without a pipeline drain. Every wave has a
-// part of every target (task_part).
+// streamed through one double-buffered pipeline: the next chunk of a
+// delivery is loaded while the current one is on MFMA. At a delivery's end
+// its result is stored first, and only then are the next delivery's first
+// chunk and old target values loaded: stores queued behind loads wait for
+// the memory pipeline, which costs more than the one exposed load latency.
+// Every wave has a part of every target (task_part).
 template <int NI, int NJ>
 __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& sm) {
   constexpr int NR = NI == 4 && NJ == 4 ? 2 : NI == 2 && NJ == 4 ? 2 : 1;  // target rows in tiles
@@ -283,7 +285,6 @@ __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& 
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   d4 acc[4][4];
   TaskOp T = task_op(a, tk[0]);
-  TaskOp Tn = T;
   int rb, cb;
   task_part(T, w, rb, cb);
   task_issue(T, 0, sm.buf[0], w, l);
@@ -291,14 +292,9 @@ __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& 
   int idx = 0, c = 0, p = 0;
   for (;;) {
     const bool last = c + 1 == T.nch;
-    if (!last) {
-      task_issue(T, c + 1, sm.buf[p ^ 1], w, l);
-    } else if (idx + 1 < n) {
-      Tn = task_op(a, tk[idx + 1]);
-      task_issue(Tn, 0, sm.buf[p ^ 1], w, l);
-    }
+    if (!last) task_issue(T, c + 1, sm.buf[p ^ 1], w, l);
     // chunk c has landed
-    if (!last || idx + 1 < n) {
+    if (!last) {
       if constexpr (NL == 16) __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16)
       else __builtin_amdgcn_s_waitcnt(0x0f7c);                     // vmcnt(12)
     } else {
@@ -315,8 +311,9 @@ __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& 
     if (last) {
       task_store<NI, NJ>(acc, T, rb, cb, l);
       if (++idx == n) break;
-      T = Tn;
+      T = task_op(a, tk[idx]);
       c = 0;
+      task_issue(T, 0, sm.buf[p], w, l);
       task_init<NI, NJ>(acc, T, rb, cb, l);
     } else {
       ++c;
