@@ -164,13 +164,15 @@ __device__ __forceinline__ int task_loads(const TaskOp& T) { return 8 + 4 * T.nr
 // load. Lane l of a left-operand load takes the 16-byte piece
 // (l & 15) ^ (l >> 4) of row 4j + (l >> 4); of a right-operand load the
 // columns 2l, 2l+1 (clamped to the target: never used past it).
-__device__ __forceinline__ void task_issue(const TaskOp& T, int c, TaskChunk& d, int w, int l) {
+// (i0, i1 select the part i0 <= i < i1 of the loads)
+__device__ __forceinline__ void task_issue(const TaskOp& T, int c, TaskChunk& d, int w, int l, int i0 = 0,
+                                           int i1 = 8) {
   const int ar = l >> 4, ap = (l & 15) ^ ar;
   const double* ac = T.A + (int64_t)(c >> 1) * 4096 + (c & 1) * 2048;
   const int col = min(2 * l, TB * T.nc - 2);
   const double* pb = T.B + (int64_t)(c >> 1) * T.bks + (c & 1) * 32 * TB + (col >> 6) * 4096 + (col & 63);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = i0; i < i1; ++i) {
     const int j = w + 4 * i;
     if (i < 4 * T.nr) {
       const double* pa = ac + (j >> 4) * T.ars + (4 * (j & 15) + ar) * 32 + 2 * ap;
@@ -237,8 +239,8 @@ __device__ __forceinline__ void task_store(const d4 (&acc)[4][4], const TaskOp& 
 // One staged chunk on MFMA: acc[i][j] += A(rows rb + 16 i ..) B(cols cb + 16 j ..).
 // The operands of k-step kk + 1 are read while kk is on MFMA (two register
 // sets), the reads spread between the MFMAs.
-template <int NI, int NJ>
-__device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, int rb, int cb, int l) {
+template <int NI, int NJ, typename Mid>
+__device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, int rb, int cb, int l, Mid&& mid) {
   const int r0 = l & 15, rr = r0 & 3;
   double av[2][NI], bv[2][NJ];
 #pragma unroll
@@ -251,6 +253,12 @@ __device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, i
       for (int i = 0; i < NI; ++i) av[nx][i] = st.a[(rb + 16 * i + r0) >> 2][ao];
 #pragma unroll
       for (int j = 0; j < NJ; ++j) bv[nx][j] = st.b[k][cb + 16 * j + r0];
+    }
+    if (kk == KQ / 8) {
+      // half-way: the rest of the next chunk's loads
+      __builtin_amdgcn_sched_barrier(0);
+      mid();
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (kk >= 0) {
       const int cur = kk & 1;
@@ -292,18 +300,19 @@ __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& 
   int idx = 0, c = 0, p = 0;
   for (;;) {
     const bool last = c + 1 == T.nch;
-    if (!last) task_issue(T, c + 1, sm.buf[p ^ 1], w, l);
-    // chunk c has landed
-    if (!last) {
-      if constexpr (NL == 16) __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16)
-      else __builtin_amdgcn_s_waitcnt(0x0f7c);                     // vmcnt(12)
-    } else {
-      __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
-    }
+    // the next chunk's loads go out in two halves, the second one half-way
+    // through this chunk's MFMAs (one batch of them stalls this wave's issue
+    // until the memory pipeline takes it)
+    if (!last) task_issue(T, c + 1, sm.buf[p ^ 1], w, l, 0, 4);
+    // chunk c has landed (issued after it: the first half of the next, 8 loads)
+    if (!last) __builtin_amdgcn_s_waitcnt(0x0f78);  // vmcnt(8)
+    else __builtin_amdgcn_s_waitcnt(0x0f70);        // vmcnt(0)
     // a bare barrier: the wait above already covers this wave's part of
     // chunk c, and a fenced barrier would also wait for the next chunk
     asm volatile("s_barrier" ::: "memory");
-    task_mma<NI, NJ>(acc, sm.buf[p], rb, cb, l);
+    task_mma<NI, NJ>(acc, sm.buf[p], rb, cb, l, [&]() {
+      if (!last) task_issue(T, c + 1, sm.buf[p ^ 1], w, l, 4, 8);
+    });
     // buffer p is refilled next: every wave's reads of it are complete
     // before the barrier, while the next chunk stays in flight
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
