@@ -221,13 +221,14 @@ __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f, const T* A, int64_t
   }
 }
 
+// (i0, i1 select the part i0 <= i < i1 of the loads)
 __device__ __forceinline__ void gram_issue(const double* Sp, const double* Sq, int64_t ld, int c,
-                                           GramChunk& g, int w, int l) {
+                                           GramChunk& g, int w, int l, int i0 = 0, int i1 = 8) {
   typedef __attribute__((address_space(3))) void lds_v;
   const int ar = l >> 4, ap = (l & 15) ^ ar;
   const int64_t k0 = (int64_t)c * GQ + 2 * ap;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = i0; i < i1; ++i) {
     const int j = w + 4 * i;
     const int64_t ro = (int64_t)(4 * j + ar) * ld + k0;
     __builtin_amdgcn_global_load_lds((const void*)(Sp + ro), (lds_v*)&g.a[j][0], 16, 0, 0);
@@ -272,9 +273,13 @@ __device__ __forceinline__ void gram_part(const Side& sd, int bp, int bq, int c0
   gram_issue(Sp, Sq, d, c0, buf[0], w, l);
   for (int c = c0; c < c1; ++c) {
     const int cb = (c - c0) & 1;
-    if (c + 1 < c1) {
-      gram_issue(Sp, Sq, d, c + 1, buf[cb ^ 1], w, l);
-      __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16): chunk c has landed
+    // the next chunk's loads in two halves, the second half-way through this
+    // chunk's MFMAs (one batch stalls the wave's issue until the memory
+    // pipeline takes it)
+    const bool more = c + 1 < c1;
+    if (more) {
+      gram_issue(Sp, Sq, d, c + 1, buf[cb ^ 1], w, l, 0, 4);
+      __builtin_amdgcn_s_waitcnt(0x0f78);  // vmcnt(8): chunk c has landed
     } else {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
@@ -293,6 +298,11 @@ __device__ __forceinline__ void gram_part(const Side& sd, int bp, int bq, int c0
 #pragma unroll
     for (int kk = 0; kk < GQ / 4; ++kk) {
       const int cur = kk & 1, nx = cur ^ 1;
+      if (kk == GQ / 8 && more) {
+        __builtin_amdgcn_sched_barrier(0);
+        gram_issue(Sp, Sq, d, c + 1, buf[cb ^ 1], w, l, 4, 8);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if (kk + 1 < GQ / 4) {
         const int kp = 2 * (kk + 1) + (l >> 5), ao = GQ * rr + 2 * (kp ^ rr) + ((l >> 4) & 1);
 #pragma unroll
@@ -819,14 +829,16 @@ struct UpdChunk {
   };
 };
 
+// (i0, i1 select the part i0 <= i < i1 of the loads)
 template <int BT>
 __device__ __forceinline__ void upd_issue(const double* Ap, int64_t lda, const double* Bp, int64_t ldb,
-                                          int c, int nr, int nc, UpdChunk& d, int w, int l) {
+                                          int c, int nr, int nc, UpdChunk& d, int w, int l, int i0 = 0,
+                                          int i1 = 8) {
   typedef __attribute__((address_space(3))) void lds_v;
   const int ar = l >> 4, ap = (l & 15) ^ ar;
   const int64_t k0 = (int64_t)c * GQ;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = i0; i < i1; ++i) {
     const int j = w + 4 * i;
     const double* pa = Ap + (int64_t)min(4 * j + ar, TB * nr - 1) * lda + k0 + 2 * ap;
     __builtin_amdgcn_global_load_lds((const void*)pa, (lds_v*)&d.a[j][0], 16, 0, 0);
@@ -866,9 +878,13 @@ __device__ void upd_tile(double* out, int64_t ldo, const double* Ap, int64_t lda
   }
   const int nch = K / GQ;
   for (int c = 0; c < nch; ++c) {
-    if (c + 1 < nch) {
-      upd_issue<BT>(Ap, lda, Bp, ldb, c + 1, nr, nc, buf[(c + 1) & 1], w, l);
-      __builtin_amdgcn_s_waitcnt(0x4f70);  // vmcnt(16): chunk c has landed
+    // the next chunk's loads in two halves, the second half-way through this
+    // chunk's MFMAs (one batch stalls the wave's issue until the memory
+    // pipeline takes it)
+    const bool more = c + 1 < nch;
+    if (more) {
+      upd_issue<BT>(Ap, lda, Bp, ldb, c + 1, nr, nc, buf[(c + 1) & 1], w, l, 0, 4);
+      __builtin_amdgcn_s_waitcnt(0x0f78);  // vmcnt(8): chunk c has landed
     } else {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
@@ -878,6 +894,11 @@ __device__ void upd_tile(double* out, int64_t ldo, const double* Ap, int64_t lda
 #pragma unroll
     for (int kk = -1; kk < GQ / 4; ++kk) {
       const int nx = (kk + 1) & 1;
+      if (kk == GQ / 8 && more) {
+        __builtin_amdgcn_sched_barrier(0);
+        upd_issue<BT>(Ap, lda, Bp, ldb, c + 1, nr, nc, buf[(c + 1) & 1], w, l, 4, 8);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       if (kk + 1 < GQ / 4) {
         const int k = 4 * (kk + 1) + (l >> 4), kp = 2 * (kk + 1) + (l >> 5);
         const int ao = GQ * rr + 2 * (kp ^ rr) + ((l >> 4) & 1);
