@@ -153,10 +153,6 @@ __device__ __forceinline__ TaskOp task_op(const StageArgs& a, int4 tk) {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Load instructions per wave for one chunk of T: eight right-operand rows and
-// 4 nr left-operand row blocks.
-__device__ __forceinline__ int task_loads(const TaskOp& T) { return 8 + 4 * T.nr; }
-
 // Chunk c of task T into d (source tile c / 2, its columns (rows of B)
 // 32 (c % 2) ..): wave w moves the left-operand row blocks j = w + 4i (rows
 // 4j .. 4j+3, i < 4 nr: 1 KB of contiguous memory in S order) and the
@@ -238,9 +234,11 @@ __device__ __forceinline__ void task_store(const d4 (&acc)[4][4], const TaskOp& 
 
 // One staged chunk on MFMA: acc[i][j] += A(rows rb + 16 i ..) B(cols cb + 16 j ..).
 // The operands of k-step kk + 1 are read while kk is on MFMA (two register
-// sets), the reads spread between the MFMAs.
+// sets), the reads spread between the MFMAs; mid() runs half-way (before the
+// MFMAs of k-step KQ / 8).
 template <int NI, int NJ, typename Mid>
-__device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, int rb, int cb, int l, Mid&& mid) {
+__device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, int rb, int cb, int l,
+                                         Mid&& mid) {
   const int r0 = l & 15, rr = r0 & 3;
   double av[2][NI], bv[2][NJ];
 #pragma unroll
@@ -288,8 +286,6 @@ __device__ __forceinline__ void task_mma(d4 (&acc)[4][4], const TaskChunk& st, i
 // Every wave has a part of every target (task_part).
 template <int NI, int NJ>
 __device__ void run_stream(const StageArgs& a, const int4* tk, int n, TaskSmem& sm) {
-  constexpr int NR = NI == 4 && NJ == 4 ? 2 : NI == 2 && NJ == 4 ? 2 : 1;  // target rows in tiles
-  constexpr int NL = 8 + 4 * NR;  // load instructions per wave and chunk
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
   d4 acc[4][4];
   TaskOp T = task_op(a, tk[0]);
