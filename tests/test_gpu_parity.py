@@ -25,7 +25,10 @@ def _factor_close(got, ref, tol):
     assert err <= tol, err
 
 
-@pytest.mark.parametrize("m,n", [(1, 1), (5, 7), (63, 65), (130, 200), (256, 320), (384, 128), (600, 520)])
+# (384, 128) and (640, 384): Gram tiles split between two work groups, ranges
+# across the two sides; (320, 512): only the second side on 128-wide tiles
+@pytest.mark.parametrize("m,n", [(1, 1), (5, 7), (63, 65), (130, 200), (256, 320), (384, 128), (600, 520),
+                                 (640, 384), (320, 512)])
 @pytest.mark.parametrize("dtype", ["f64", "f32"])
 def test_factors_match_oracle(m, n, dtype):
     p = wl.random_problem(m, n, 1, dtype, "wishart")
