@@ -88,6 +88,27 @@ def test_end_to_end(m, n, kind):
     pr.property_checks(p, res)
 
 
+@pytest.mark.parametrize("m,n,dtype", [(1000, 700, "f32"), (700, 1000, "f64"), (2085, 1547, "f32")])
+def test_mid_size_full_replay(m, n, dtype):
+    """Ragged mid-size problems (16 x 11, 11 x 16 and 33 x 25 tiles: far batches onto
+    2 x 2 super-tiles, near deliveries of every shape, edge tiles): the whole
+    sweep replayed by the oracle with the GPU's factors, then the oracle's own
+    factors and the objective."""
+    p = wl.random_problem(m, n, 11, dtype, "wishart")
+    X, A, B = p.widened()
+    print(f"[mid] {m}x{n} {dtype}: GPU factor + sweep", flush=True)
+    res = pr.gpu_run(p)
+    Zo, Yo, c, hard = pr.replay(p, res["L"], res["U"], res["Z"])
+    pr.assert_replay_pass(p, c, hard, m * n)
+    tol = 1e-9 if dtype == "f64" else 2e-6 * max(1.0, np.abs(Yo).max())
+    assert np.abs(res["Y"] - Yo).max() <= tol
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zo3, Yo3, c3, hard3 = pr.replay(p, L, U, res["Z"])
+    pr.assert_replay_pass(p, c3, hard3, m * n)
+    pr.assert_objective(p, res["obj"], oracle.objective(X, Zo3, A, B))
+    pr.property_checks(p, res)
+
+
 @pytest.mark.parametrize("kind", ["diag", "identity_right", "identity_left", "lower"])
 def test_special_bases(kind):
     p = wl.random_problem(97, 131, 6, "f64", kind)
