@@ -21,6 +21,10 @@ This module is argument marshalling around ``oracle.c`` (plain C, fp64):
 * ``round_gptq2d``                -- Algorithm 3 (Sec. 4.2)
 * ``round_implicit``              -- Algorithm 6 (Appendix B)
 * ``objective``                   -- ||A (Z - X) B||_F^2 by definition
+* ``round_reverse``               -- the same rounding in reverse order (from the
+                                     last row and column, the direction of YAQA,
+                                     Sec. 2): Algorithm 5 on the index-reversed
+                                     problem (P X P, A P, P B), reversed back
 
 Every sweep returns ``(Z, Ypre, counts, hard)``: the rounded matrix (int32),
 the value each entry had when it was rounded, the synchronised-replay counters
@@ -277,3 +281,28 @@ def objective(X, Z, A, B) -> float:
     B = _d(B)
     m, n = X.shape
     return float(_load().orc_objective(m, n, _dp(X), _ip(Z), _dp(A), _dp(B)))
+
+
+def reverse_problem(X, A, B):
+    """The index-reversed problem (P X P, A P, P B), P the reversal
+    permutation: ||A (Z - X) B|| = ||(A P)(P Z P - P X P)(P B)||, so rounding it
+    forward rounds the original from its last row and column."""
+    X = _d(X)
+    A = _d(A)
+    B = _d(B)
+    return (np.ascontiguousarray(X[::-1, ::-1]), np.ascontiguousarray(A[:, ::-1]),
+            np.ascontiguousarray(B[::-1, :]))
+
+
+def round_reverse(X, A, B, hint=None, tau=0.0, hard_cap=64):
+    """Two-sided rounding in reverse order (Sec. 2: YAQA's direction): the
+    factors and Algorithm 5 of the index-reversed problem, Z and the values
+    rounded from reversed back. A hint is given in the original order."""
+    Xr, Ar, Br = reverse_problem(X, A, B)
+    L, lamL, U, lamU = factors(Ar, Br)
+    h = None if hint is None else np.ascontiguousarray(np.asarray(hint)[::-1, ::-1])
+    Z, Y, c, hard = round_nested(Xr, L, U, hint=h, tau=tau, hard_cap=hard_cap)
+    m, n = Z.shape
+    # flat indices of hard mismatches in the original order
+    hard = np.array([(m - 1 - k // n) * n + (n - 1 - k % n) for k in hard], dtype=np.int64)
+    return np.ascontiguousarray(Z[::-1, ::-1]), np.ascontiguousarray(Y[::-1, ::-1]), c, hard

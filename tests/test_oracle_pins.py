@@ -250,6 +250,73 @@ def test_greedy_bruteforce(m, n, seed):
     assert np.array_equal(Zc, Zb)
 
 
+def _greedy_bruteforce_order(X, A, B, order):
+    """Babai's greedy over the coordinates of vec(X) (column-major) in the
+    given order: each is the integer minimising the objective with the
+    earlier ones (in that order) fixed and the later ones free."""
+    m, n = X.shape
+    K = _kron_metric(A, B)
+    x = X.reshape(-1, order="F")
+    d = m * n
+    P = np.asarray(order)
+    Kp = K[np.ix_(P, P)]
+    xp = x[P]
+    z = np.zeros(d)
+    for k in range(d):
+        a = np.arange(k + 1)
+        b = np.arange(k + 1, d)
+        S = Kp[np.ix_(a, a)]
+        if len(b):
+            S = S - Kp[np.ix_(a, b)] @ np.linalg.solve(Kp[np.ix_(b, b)], Kp[np.ix_(b, a)])
+        r_prev = z[:k] - xp[:k]
+
+        def f(t):
+            r = np.append(r_prev, t - xp[k])
+            return r @ S @ r
+
+        cont = xp[k] - (S[k, :k] @ r_prev) / S[k, k]
+        cands = np.arange(np.floor(cont) - 2, np.ceil(cont) + 3)
+        vals = np.array([f(t) for t in cands])
+        best = cands[np.isclose(vals, vals.min(), rtol=1e-12, atol=1e-12)]
+        z[k] = best[0] if len(best) == 1 else best[best % 2 == 0][0]
+    out = np.empty(d)
+    out[P] = z
+    return out.reshape(m, n, order="F").astype(np.int32)
+
+
+@pytest.mark.parametrize("m,n", [(2, 3), (3, 2), (3, 3)])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_reverse_order_bruteforce(m, n, seed):
+    """The reverse-order rounding (from the last row and column, Sec. 2) is
+    Babai's greedy visiting vec(X) from its last coordinate to its first, on
+    the original problem (no index reversal in the brute force)."""
+    X, A, B = _prob(m, n, 70 + seed, "general")
+    Zb = _greedy_bruteforce_order(X, A, B, list(range(m * n))[::-1])
+    Zr, Yr, c, hard = oracle.round_reverse(X, A, B)
+    assert np.array_equal(Zr, Zb)
+    # and the forward order of the same routine is the existing forward oracle
+    Zf = _greedy_bruteforce_order(X, A, B, list(range(m * n)))
+    L, lamL, U, lamU = oracle.factors(A, B)
+    assert np.array_equal(oracle.round_nested(X, L, U)[0], Zf)
+
+
+def test_reverse_order_differs_and_is_consistent():
+    """On a generic problem the two directions round differently, and each
+    satisfies its own identity: the reverse-order Z is the forward rounding of
+    the index-reversed problem, |E| <= 1/2 there, and the objective is
+    invariant under the reindexing."""
+    X, A, B = _prob(9, 7, 81, "general")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zf = oracle.round_nested(X, L, U)[0]
+    Zr, Yr, c, hard = oracle.round_reverse(X, A, B)
+    assert not np.array_equal(Zf, Zr)
+    Xr, Ar, Br = oracle.reverse_problem(X, A, B)
+    assert abs(oracle.objective(Xr, Zr[::-1, ::-1], Ar, Br) - oracle.objective(X, Zr, A, B)) <= \
+        1e-9 * oracle.objective(X, Zr, A, B)
+    assert np.abs(np.rint(Yr) - Yr).max() <= 0.5
+    assert np.array_equal(np.rint(Yr).astype(np.int32), Zr)
+
+
 def test_kron_metric_matches_definition():
     X, A, B = _prob(3, 4, 1, "general")
     K = _kron_metric(A, B)
