@@ -91,20 +91,24 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(prob, sample: int):
+def cpu_baseline(prob, sample: int, reverse: bool = False):
     """The oracle as it stands (Algorithm 5 sweep, explicit-inverse + LDL
-    factors) on the leading sample x sample block of the workload, scaled by
-    the flop count to the full problem."""
+    factors; in reverse order the same on the index-reversed block) on the
+    leading sample x sample block of the workload, scaled by the flop count
+    to the full problem."""
     import numpy as np
 
     import oracle
 
     X, A, B = prob.widened()
     s_m, s_n = min(sample, prob.m), min(sample, prob.n)
+    Xs, As, Bs = np.ascontiguousarray(X[:s_m, :s_n]), A[:s_m, :s_m], B[:s_n, :s_n]
+    if reverse:
+        Xs, As, Bs = oracle.reverse_problem(Xs, As, Bs)
     t0 = time.perf_counter()
-    L, lamL, U, lamU = oracle.factors(A[:s_m, :s_m], B[:s_n, :s_n])
+    L, lamL, U, lamU = oracle.factors(As, Bs)
     t1 = time.perf_counter()
-    oracle.round_nested(np.ascontiguousarray(X[:s_m, :s_n]), L, U)
+    oracle.round_nested(Xs, L, U)
     t2 = time.perf_counter()
     tf, tr = t1 - t0, t2 - t1
     m, n = prob.m, prob.n
@@ -144,6 +148,8 @@ def main():
     ap.add_argument("--dtype", default=None)
     ap.add_argument("--cpu-sample", type=int, default=1536)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--order", choices=["forward", "reverse"], default="forward",
+                    help="rounding order: from the first row and column on, or from the last")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run a plain MIB-MiB device copy first (counter calibration)")
     args = ap.parse_args()
@@ -174,7 +180,7 @@ def main():
     X = torch.from_numpy(prob.X).to(dev)
     A = torch.from_numpy(prob.A).to(dev)
     B = torch.from_numpy(prob.B).to(dev)
-    f = binding.Factors(m, n)
+    f = binding.Factors(m, n, reverse=args.order == "reverse")
     ws = f.workspace()
     Z = torch.empty((m, n), dtype=torch.int32, device=dev)
     Y = torch.empty((m, n), dtype=X.dtype, device=dev)
@@ -253,10 +259,11 @@ def main():
         "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": f"c{args.config}: {WORKLOADS[args.config]}", "m": m, "n": n,
-                   "io_dtype": prob.dtype},
+                   "io_dtype": prob.dtype, "order": args.order},
         "roofline": {
             "bound": "mfma", "achieved": achieved, "peak": PEAK_F64_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_F64_TFLOPS, "traffic": stage_traffic(args.config, prob.dtype),
+            "frac": achieved / PEAK_F64_TFLOPS, "traffic": (stage_traffic(args.config, prob.dtype)
+                                                          if args.order == "forward" else None),
             "frac_of_fp32_peak_reference": achieved / PEAK_F32_TFLOPS,
             "kernel": "k_stage (sweep stage: in-tile rounding + deferred-feedback GEMM tasks)",
             "flop_per_launch": per_launch, "launches_per_step": stages,
@@ -274,7 +281,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log(f"cpu baseline on a {args.cpu_sample} sample")
-        out["cpu_baseline"] = cpu_baseline(prob, args.cpu_sample)
+        out["cpu_baseline"] = cpu_baseline(prob, args.cpu_sample, args.order == "reverse")
     print(json.dumps(out), flush=True)
 
 

@@ -76,6 +76,21 @@ void gptq2d_factors_destroy(gptq2d_factors_t f);
 /* Problem shape of a handle. */
 gptq2d_status gptq2d_factors_shape(gptq2d_factors_t f, int* m, int* n);
 
+/* Rounding order of handle f. The paper's sweep visits vec(X) from its first
+ * entry on (GPTQ's direction); Sec. 2 notes that YAQA rounds in the opposite
+ * direction, from the last column on. reverse = 0 (the default) selects the
+ * first, reverse != 0 the second: the entries are visited in the reverse of
+ * the forward order, which is the forward sweep of the index-reversed problem
+ * (P X P, A P, P B; P the reversal permutation of matching size) with its Z
+ * and Y reversed back. Z, Y and the objective are returned in X's own
+ * indexing either way. The factors a handle holds belong to its order: in
+ * reverse order they are those of the index-reversed problem, and
+ * gptq2d_factors_export / gptq2d_factors_import exchange them in that form.
+ * Set the order before gptq2d_factor_compute or gptq2d_factors_import;
+ * factors already in the handle are not converted. Enqueues nothing.
+ * Errors: INVALID_ARG on a NULL handle. */
+gptq2d_status gptq2d_factors_set_order(gptq2d_factors_t f, int reverse);
+
 /* Enqueues the factorisation of A (m x m, lda) and B (n x n, ldb), both of
  * type dt, into f: Gram formation, Cholesky of the index-reversed Grams,
  * triangular inversion and normalisation (the LDL factors of the inverse

@@ -55,6 +55,7 @@ def load():
         "gptq2d_factors_create": (i32, [i32, i32, ctypes.POINTER(vp)]),
         "gptq2d_factors_destroy": (None, [vp]),
         "gptq2d_factors_shape": (i32, [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]),
+        "gptq2d_factors_set_order": (i32, [vp, i32]),
         "gptq2d_factor_compute": (i32, [vp, i32, vp, i64, vp, i64, vp]),
         "gptq2d_factor_check": (i32, [vp, vp]),
         "gptq2d_factor": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, ctypes.POINTER(vp)]),
@@ -143,6 +144,11 @@ def gptq2d_factors_shape(h: int):
     _check(load().gptq2d_factors_shape(ctypes.c_void_p(h), ctypes.byref(m), ctypes.byref(n)),
            "gptq2d_factors_shape")
     return m.value, n.value
+
+
+def gptq2d_factors_set_order(h: int, reverse: bool) -> None:
+    _check(load().gptq2d_factors_set_order(ctypes.c_void_p(h), int(bool(reverse))),
+           "gptq2d_factors_set_order")
 
 
 def gptq2d_factor_compute(h: int, A: torch.Tensor, B: torch.Tensor, stream=None) -> None:
@@ -259,13 +265,19 @@ def gptq2d_schedule_tasks(m: int, n: int, g: int):
 class Factors:
     """Owning wrapper of a factor handle."""
 
-    def __init__(self, m: int, n: int):
+    def __init__(self, m: int, n: int, reverse: bool = False):
+        """reverse: round from the last row and column on (the factors are then
+        those of the index-reversed problem)."""
         self.m, self.n = m, n
         self.handle = gptq2d_factors_create(m, n)
+        self.reverse = bool(reverse)
+        if self.reverse:
+            gptq2d_factors_set_order(self.handle, True)
 
     @classmethod
-    def from_bases(cls, A: torch.Tensor, B: torch.Tensor, check: bool = True, stream=None):
-        f = cls(A.shape[0], B.shape[0])
+    def from_bases(cls, A: torch.Tensor, B: torch.Tensor, check: bool = True, stream=None,
+                   reverse: bool = False):
+        f = cls(A.shape[0], B.shape[0], reverse)
         f.compute(A, B, stream)
         if check:
             gptq2d_factor_check(f.handle, stream)

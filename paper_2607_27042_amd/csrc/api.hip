@@ -154,6 +154,12 @@ gptq2d_status gptq2d_factors_shape(gptq2d_factors_t f, int* m, int* n) {
   return GPTQ2D_OK;
 }
 
+gptq2d_status gptq2d_factors_set_order(gptq2d_factors_t f, int reverse) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  f->rev = reverse ? 1 : 0;
+  return GPTQ2D_OK;
+}
+
 gptq2d_status gptq2d_factor_compute(gptq2d_factors_t f, gptq2d_dtype dt, const void* A,
                                     int64_t lda, const void* B, int64_t ldb, void* stream) {
   if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");

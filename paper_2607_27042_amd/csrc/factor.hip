@@ -38,6 +38,7 @@ struct Side {
 struct FacArgs {
   Side s[2];
   int* flags;
+  int rev;  // reverse order: the index-reversed problem (A P, P B), so no reversal below
 };
 
 // Lower-triangle enumeration of tile pairs: b -> (i, j) with i >= j.
@@ -82,7 +83,8 @@ __device__ __forceinline__ void gemm64(Acc& acc, const double* pa, int64_t lda, 
 // ---------------------------------------------------------------------------
 
 template <typename T, int SIDE>
-__device__ __forceinline__ void gram_load(const T* S, int64_t ld, int d, int i0, int k0, double r[16]) {
+__device__ __forceinline__ void gram_load(const T* S, int64_t ld, int d, int i0, int k0, double r[16],
+                                          int rev) {
   const int t = threadIdx.x;
   T v[16];
   bool ok[16];
@@ -92,14 +94,15 @@ __device__ __forceinline__ void gram_load(const T* S, int64_t ld, int d, int i0,
   for (int s = 0; s < 16; ++s) {
     const int e = t + NT * s, hi = e >> 6, lo = e & 63;
     int64_t off;
+    // (in reverse order the problem is (A P, P B): A[k][idx], B[idx][k])
     if (SIDE == 0) {  // (k = hi, i = lo): A[k0+k][d-1-(i0+i)], coalesced along i
       const int k = k0 + hi, idx = i0 + lo;
       ok[s] = k < d && idx < d;
-      off = (int64_t)k * ld + (d - 1 - idx);
+      off = (int64_t)k * ld + (rev ? idx : d - 1 - idx);
     } else {          // (i = hi, k = lo): B[d-1-(i0+i)][k0+k], coalesced along k
       const int idx = i0 + hi, k = k0 + lo;
       ok[s] = k < d && idx < d;
-      off = (int64_t)(d - 1 - idx) * ld + k;
+      off = (int64_t)(rev ? idx : d - 1 - idx) * ld + k;
     }
     v[s] = S[ok[s] ? off : 0];
   }
@@ -108,12 +111,12 @@ __device__ __forceinline__ void gram_load(const T* S, int64_t ld, int d, int i0,
 }
 
 template <typename T, int SIDE>
-__device__ void gram_tile(const Side& sd, const T* S, int64_t ld, int bp, int bq, Stage64& st) {
+__device__ void gram_tile(const Side& sd, const T* S, int64_t ld, int bp, int bq, Stage64& st, int rev) {
   Acc acc;
   acc.zero();
   double ra[16], rb[16];
-  gram_load<T, SIDE>(S, ld, sd.d, bp * TB, 0, ra);
-  gram_load<T, SIDE>(S, ld, sd.d, bq * TB, 0, rb);
+  gram_load<T, SIDE>(S, ld, sd.d, bp * TB, 0, ra, rev);
+  gram_load<T, SIDE>(S, ld, sd.d, bq * TB, 0, rb, rev);
   const int nk = (sd.d + TB - 1) / TB;
   for (int kb = 0; kb < nk; ++kb) {
     if (SIDE == 0) {
@@ -125,8 +128,8 @@ __device__ void gram_tile(const Side& sd, const T* S, int64_t ld, int bp, int bq
     }
     __syncthreads();
     if (kb + 1 < nk) {  // next block's loads in flight during this block's MFMAs
-      gram_load<T, SIDE>(S, ld, sd.d, bp * TB, (kb + 1) * TB, ra);
-      gram_load<T, SIDE>(S, ld, sd.d, bq * TB, (kb + 1) * TB, rb);
+      gram_load<T, SIDE>(S, ld, sd.d, bp * TB, (kb + 1) * TB, ra, rev);
+      gram_load<T, SIDE>(S, ld, sd.d, bq * TB, (kb + 1) * TB, rb, rev);
     }
     mma_blk(acc, st);
     __syncthreads();
@@ -154,10 +157,10 @@ __global__ __launch_bounds__(NT) void k_gram(FacArgs f, const T* A, int64_t lda,
   int bp, bq;
   if ((int)blockIdx.x < t0) {
     tri_index(blockIdx.x, bp, bq);
-    gram_tile<T, 0>(f.s[0], A, lda, bp, bq, st);
+    gram_tile<T, 0>(f.s[0], A, lda, bp, bq, st, f.rev);
   } else {
     tri_index(blockIdx.x - t0, bp, bq);
-    gram_tile<T, 1>(f.s[1], B, ldb, bp, bq, st);
+    gram_tile<T, 1>(f.s[1], B, ldb, bp, bq, st, f.rev);
   }
 }
 
@@ -166,8 +169,10 @@ __global__ __launch_bounds__(NT) void k_gram(FacArgs f, const T* A, int64_t lda,
 //
 // k_gram_prep writes, widened to fp64, the row-major panel S (d x d, row
 // stride d) whose rows are the reversed Gram indices: S[p][k] = A[k][d-1-p]
-// (side 0, a transpose through LDS) or B[d-1-p][k] (side 1). The panel lives
-// in the side's inverse buffer, which the factorisation fills only later.
+// (side 0, a transpose through LDS) or B[d-1-p][k] (side 1); in reverse order
+// the problem is already the index-reversed one, S[p][k] = A[k][p] or B[p][k].
+// The panel lives in the side's inverse buffer, which the factorisation fills
+// only later.
 //
 // k_gram128 then forms Gr[p][q] = sum_k S[p][k] S[q][k] on the lower
 // 128 x 128 tiles: four waves, each a 64 x 64 quadrant as 4 x 4 MFMA blocks
@@ -198,25 +203,29 @@ __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f, const T* A, int64_t
   const int i0 = (b / nt) * TB, k0 = (b % nt) * TB;  // S rows i0.., columns k0..
   double* S = sd.li;
   const int t = threadIdx.x;
+  const int rev = f.rev;
   if (side == 0) {
-    // A rows k0 + r, columns d-1-(i0+63) .. d-1-i0 (ascending), coalesced
+    // A rows k0 + r, columns d-1-(i0+63) .. d-1-i0 (ascending; in reverse
+    // order i0 .. i0+63), coalesced
+    const int c0 = rev ? i0 : d - i0 - TB;
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const int e = t + NT * u, r = e >> 6, c = e & 63;  // c: column offset in A
-      tile[r][c] = (double)A[(int64_t)(k0 + r) * lda + (d - i0 - TB) + c];
+      tile[r][c] = (double)A[(int64_t)(k0 + r) * lda + c0 + c];
     }
     __syncthreads();
-    // S[i0 + i][k0 + k] = A[k0 + k][d-1-(i0+i)] = tile[k][63 - i]
+    // S[i0 + i][k0 + k] = A[k0 + k][d-1-(i0+i)] = tile[k][63 - i] (reverse order: tile[k][i])
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const int e = t + NT * u, i = e >> 6, k = e & 63;
-      S[(int64_t)(i0 + i) * d + k0 + k] = tile[k][TB - 1 - i];
+      S[(int64_t)(i0 + i) * d + k0 + k] = tile[k][rev ? i : TB - 1 - i];
     }
   } else {
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const int e = t + NT * u, i = e >> 6, k = e & 63;
-      S[(int64_t)(i0 + i) * d + k0 + k] = (double)B[(int64_t)(d - 1 - (i0 + i)) * ldb + k0 + k];
+      const int row = rev ? i0 + i : d - 1 - (i0 + i);
+      S[(int64_t)(i0 + i) * d + k0 + k] = (double)B[(int64_t)row * ldb + k0 + k];
     }
   }
 }
@@ -1087,6 +1096,7 @@ static FacArgs fac_args(Factors& f) {
     sd.nb = sd.dp / TB;
   }
   a.flags = f.flags;
+  a.rev = f.rev;
   return a;
 }
 

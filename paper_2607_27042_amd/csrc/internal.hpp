@@ -31,6 +31,9 @@ struct Factors {
   int mp = 0, np = 0;   // padded to multiples of 64
   int MT = 0, NT = 0;   // tile counts
   int device = 0;
+  // rounding order: 0 from the first row and column on, 1 from the last (the
+  // factors are then those of the index-reversed problem)
+  int rev = 0;
   // outputs of the factorisation (fp64, padded with an identity block)
   double* L = nullptr;   // mp x mp, tile by tile in S order; unit lower; upper tiles not kept
   double* U = nullptr;   // np x np, tile by tile in R order; unit upper; lower tiles not kept

@@ -40,12 +40,17 @@ struct StageArgs {
   const double* U;
   const double* dL;
   const double* dU;
+  // X, Z, Y at element (i, j) of the problem the sweep runs on: base + i ld +
+  // j cstep. In the forward order cstep = 1 and the bases are the matrices';
+  // in reverse order the problem is the index-reversed one, so each base is
+  // the matrix's last element, ld its negated row stride and cstep = -1.
   const void* X;
   int64_t ldx;
   int32_t* Z;
   int64_t ldz;
   void* Y;
   int64_t ldy;
+  int cstep;
   double* P;
   double* R;
   double* E;
@@ -107,9 +112,10 @@ union StageSmem {
 // X[gi][gj] widened, 0 outside the matrix; the load is unconditional (from a
 // clamped address) so that it does not serialise behind a branch.
 template <typename T>
-__device__ __forceinline__ double load_x(const T* X, int64_t ldx, int gi, int gj, int m, int n) {
+__device__ __forceinline__ double load_x(const T* X, int64_t ldx, int cstep, int gi, int gj, int m,
+                                         int n) {
   const bool ok = gi < m && gj < n;
-  const T v = X[ok ? (int64_t)gi * ldx + gj : 0];
+  const T v = X[ok ? (int64_t)gi * ldx + gj * cstep : 0];
   return ok ? (double)v : 0.0;
 }
 
@@ -524,8 +530,8 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
         if (!isfinite(yv)) bad |= FLAG_NONFINITE;
         else if (fabs(z) > 2147483647.0) bad |= FLAG_OVERFLOW;
         const double zc = fmin(fmax(z, -2147483648.0), 2147483647.0);
-        a.Z[(int64_t)gi * a.ldz + gj + j] = isfinite(zc) ? (int32_t)zc : 0;
-        if (Y) Y[(int64_t)gi * a.ldy + gj + j] = (T)yv;
+        a.Z[(int64_t)gi * a.ldz + (gj + j) * a.cstep] = isfinite(zc) ? (int32_t)zc : 0;
+        if (Y) Y[(int64_t)gi * a.ldy + (gj + j) * a.cstep] = (T)yv;
         part += ev[j] * ev[j] * b.dl[i] * dc[j];
       }
     }
@@ -578,7 +584,7 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        Rt[c][i][j] = load_x<T>(X, a.ldx, gi0 + br + i, gj0 + SS * c + 2 * q + j, a.m, a.n);
+        Rt[c][i][j] = load_x<T>(X, a.ldx, a.cstep, gi0 + br + i, gj0 + SS * c + 2 * q + j, a.m, a.n);
   double2 rv[4][2], pv[4][2];
   if (J >= 2) {
 #pragma unroll
@@ -1017,12 +1023,26 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
   a.U = f.U;
   a.dL = f.dL;
   a.dU = f.dU;
-  a.X = X;
-  a.ldx = ldx;
-  a.Z = Z;
-  a.ldz = ldz;
-  a.Y = Y;
-  a.ldy = ldy;
+  if (f.rev) {  // the index-reversed problem: X[m-1-i][n-1-j] etc.
+    const int64_t last_x = (int64_t)(f.m - 1) * ldx + (f.n - 1);
+    const int64_t last_z = (int64_t)(f.m - 1) * ldz + (f.n - 1);
+    const int64_t last_y = (int64_t)(f.m - 1) * ldy + (f.n - 1);
+    a.X = (const T*)X + last_x;
+    a.ldx = -ldx;
+    a.Z = Z + last_z;
+    a.ldz = -ldz;
+    a.Y = Y ? (void*)((T*)Y + last_y) : nullptr;
+    a.ldy = -ldy;
+    a.cstep = -1;
+  } else {
+    a.X = X;
+    a.ldx = ldx;
+    a.Z = Z;
+    a.ldz = ldz;
+    a.Y = Y;
+    a.ldy = ldy;
+    a.cstep = 1;
+  }
   a.P = ws.P;
   a.R = ws.R;
   a.E = ws.E;

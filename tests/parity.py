@@ -23,15 +23,16 @@ def to_dev(a: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def gpu_run(prob, factors=None, want_y=True):
+def gpu_run(prob, factors=None, want_y=True, reverse=False):
     """Factor (or import ``factors`` = (L, lamL, U, lamU) numpy fp64) and
-    round on the GPU. Returns a dict of numpy results."""
+    round on the GPU, in reverse order if ``reverse`` (the factors are then
+    those of the index-reversed problem). Returns a dict of numpy results."""
     X = to_dev(prob.X)
     if factors is None:
-        f = binding.Factors.from_bases(to_dev(prob.A), to_dev(prob.B))
+        f = binding.Factors.from_bases(to_dev(prob.A), to_dev(prob.B), reverse=reverse)
     else:
         L, lamL, U, lamU = factors
-        f = binding.Factors(prob.m, prob.n)
+        f = binding.Factors(prob.m, prob.n, reverse=reverse)
         f.load(to_dev(L), to_dev(U), to_dev(lamL), to_dev(lamU))
     Z, Y, obj = binding.round_matrix(f, X, want_y=want_y)
     L, U, lamL, lamU = f.export()

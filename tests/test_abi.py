@@ -41,6 +41,7 @@ def test_null_handle_is_rejected(lib):
     assert lib.gptq2d_round_workspace_size(null) == 0
     assert lib.gptq2d_stage_timing(null, 1) == -1
     assert lib.gptq2d_stage_time(null, None, None) == -1
+    assert lib.gptq2d_factors_set_order(null, 1) == -1
     out = ctypes.c_void_p()
     assert lib.gptq2d_factors_create(0, 5, ctypes.byref(out)) == -1
     assert lib.gptq2d_factors_create(5, 70000, ctypes.byref(out)) == -1

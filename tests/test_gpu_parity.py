@@ -109,6 +109,45 @@ def test_mid_size_full_replay(m, n, dtype):
     pr.property_checks(p, res)
 
 
+# (256, 384), (384, 128): both sides' Grams on the 128-wide path (the
+# reversal skipped in the panel transpose); the others take the 64-wide path
+@pytest.mark.parametrize("m,n,dtype", [(1, 1, "f64"), (5, 7, "f64"), (63, 65, "f32"), (130, 200, "f64"),
+                                       (256, 384, "f32"), (384, 128, "f64"), (700, 1000, "f32")])
+def test_reverse_order(m, n, dtype):
+    """Rounding from the last row and column on (Sec. 2, the direction of
+    YAQA): the factors are those of the index-reversed problem (A P, P B), and
+    the oracle's reverse-order rounding replays the GPU's Z in X's indexing,
+    under the oracle's own factors and under the GPU's."""
+    p = wl.random_problem(m, n, 13, dtype, "wishart")
+    X, A, B = p.widened()
+    Xr, Ar, Br = oracle.reverse_problem(X, A, B)
+    print(f"[reverse] {m}x{n} {dtype}", flush=True)
+    res = pr.gpu_run(p, reverse=True)
+    L, lamL, U, lamU = oracle.factors(Ar, Br)
+    _factor_close(res["L"], L, 1e-10)
+    _factor_close(res["U"], U, 1e-10)
+    np.testing.assert_allclose(res["lamL"], lamL, rtol=1e-10)
+    np.testing.assert_allclose(res["lamU"], lamU, rtol=1e-10)
+    tau = pr.TAU[dtype]
+    Zo, Yo, c, hard = oracle.round_reverse(X, A, B, hint=res["Z"], tau=tau)
+    pr.assert_replay_pass(p, c, hard, m * n)
+    tol = 1e-9 if dtype == "f64" else 2e-6 * max(1.0, np.abs(Yo).max())
+    assert np.abs(res["Y"] - Yo).max() <= tol
+    pr.assert_objective(p, res["obj"], oracle.objective(X, Zo, A, B))
+    # the same replay under the GPU's factors, on the reversed problem
+    Zg, Yg, cg, hardg = oracle.round_nested(Xr, res["L"], res["U"],
+                                            hint=np.ascontiguousarray(res["Z"][::-1, ::-1]), tau=tau)
+    pr.assert_replay_pass(p, cg, hardg, m * n)
+    # the sweep alone, with the oracle's factors imported into a reverse-order handle
+    res2 = pr.gpu_run(p, factors=(L, lamL, U, lamU), reverse=True)
+    Zo2, Yo2, c2, hard2 = oracle.round_reverse(X, A, B, hint=res2["Z"], tau=tau)
+    pr.assert_replay_pass(p, c2, hard2, m * n)
+    if m * n >= 4096:
+        # the two orders are different trajectories
+        fwd = pr.gpu_run(p)
+        assert not np.array_equal(fwd["Z"], res["Z"])
+
+
 @pytest.mark.parametrize("kind", ["diag", "identity_right", "identity_left", "lower"])
 def test_special_bases(kind):
     p = wl.random_problem(97, 131, 6, "f64", kind)
