@@ -139,6 +139,84 @@ def _cpu_model():
     return "unknown"
 
 
+def run_batch(args, dev):
+    """A step = gptq2d_factor_batched + gptq2d_round_batched over N problems
+    drawn from the config's recipe (layer seeds 0 .. N-1), inputs resident in
+    HBM. Prints one JSON line; value = N m n / step time."""
+    import torch
+
+    from paper_2607_27042_amd import binding, workloads as wl
+
+    N = args.batch
+    log(f"generating {N} problems of config {args.config}")
+    probs = [wl.make_config(args.config, args.dtype, layer=i) for i in range(N)]
+    m, n = probs[0].m, probs[0].n
+    Xs = [torch.from_numpy(p.X).to(dev) for p in probs]
+    As = [torch.from_numpy(p.A).to(dev) for p in probs]
+    Bs = [torch.from_numpy(p.B).to(dev) for p in probs]
+    fs = [binding.Factors(m, n, reverse=args.order == "reverse") for _ in range(N)]
+    handles = [f.handle for f in fs]
+    shapes = [(m, n)] * N
+    Zs = [torch.empty((m, n), dtype=torch.int32, device=dev) for _ in range(N)]
+    Ys = [torch.empty((m, n), dtype=Xs[0].dtype, device=dev) for _ in range(N)]
+    obj = torch.empty(N, dtype=torch.float64, device=dev)
+    ws = torch.empty(binding.gptq2d_round_batched_workspace_size(handles), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        binding.gptq2d_factor_batched(handles, As, Bs, stream, shapes=shapes)
+        if ev is not None:
+            ev[1].record(stream)
+        binding.gptq2d_round_batched(handles, Xs, Zs, Ys, obj, ws, stream, shapes=shapes)
+        if ev is not None:
+            ev[2].record(stream)
+
+    log(f"warmup {args.warmup}")
+    for _ in range(max(args.warmup, 1)):
+        step()
+    binding.gptq2d_factor_batched_check(handles, stream)
+    binding.gptq2d_round_batched_check(ws, stream)
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(args.steps):
+        step(ev[k])
+    end.record(stream)
+    torch.cuda.synchronize()
+    binding.gptq2d_round_batched_check(ws, stream)
+    ms_step = start.elapsed_time(end) / args.steps
+    t_fac = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    t_round = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    out = {
+        "metric": METRIC,
+        "value": N * m * n / (ms_step * 1e-3),
+        "unit": "entries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": f"{N} x c{args.config}: {WORKLOADS[args.config]}", "m": m, "n": n,
+                   "batch": N, "io_dtype": probs[0].dtype, "order": args.order},
+        "roofline": None,
+        "phases_ms": {"factor": t_fac, "round": t_round},
+        "round_entries_per_s": N * m * n / (t_round * 1e-3),
+        "objective_sum": float(obj.sum().cpu()),
+    }
+    print(json.dumps(out), flush=True)
+    for f in fs:
+        f.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -148,6 +226,9 @@ def main():
     ap.add_argument("--dtype", default=None)
     ap.add_argument("--cpu-sample", type=int, default=1536)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--batch", type=int, default=1, metavar="N",
+                    help="N problems of the config (the layers of one model, each with its own X "
+                         "and bases) per step, factorised and rounded by the batched entry points")
     ap.add_argument("--order", choices=["forward", "reverse"], default="forward",
                     help="rounding order: from the first row and column on, or from the last")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -169,6 +250,10 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+
+    if args.batch > 1:
+        run_batch(args, dev)
+        return
 
     if args.copy_calibration > 0:
         log(f"copy calibration: {args.copy_calibration} MiB x 3")

@@ -104,6 +104,23 @@ gptq2d_status gptq2d_factor_compute(gptq2d_factors_t f, gptq2d_dtype dt, const v
  * met a non-positive or non-finite pivot, OK otherwise. */
 gptq2d_status gptq2d_factor_check(gptq2d_factors_t f, void* stream);
 
+/* Enqueues the factorisation of `count` problems at once: problem p as
+ * gptq2d_factor_compute(f[p], dt, A[p], lda[p], B[p], ldb[p], stream) would,
+ * with the same result. f, A, lda, B, ldb are host arrays (A[p], B[p] device
+ * pointers); a handle may appear only once. The problems run side by side
+ * (each handle on a stream of its own, created on its first batched use and
+ * ordered after the work already on `stream`); `stream` waits for all of
+ * them. Small problems, whose factorisation is a chain of short launches,
+ * overlap instead of queueing behind one another. Allocates no device
+ * memory; does not synchronise. Errors: INVALID_ARG, HIP. */
+gptq2d_status gptq2d_factor_batched(int count, const gptq2d_factors_t* f, gptq2d_dtype dt,
+                                    const void* const* A, const int64_t* lda, const void* const* B,
+                                    const int64_t* ldb, void* stream);
+
+/* Synchronises `stream` and returns SINGULAR if the last factorisation of any
+ * of the handles f[0 .. count-1] met a non-positive or non-finite pivot. */
+gptq2d_status gptq2d_factor_batched_check(int count, const gptq2d_factors_t* f, void* stream);
+
 /* Convenience: create + compute + check (one synchronisation). On error no
  * handle is returned. */
 gptq2d_status gptq2d_factor(int m, int n, gptq2d_dtype dt, const void* A, int64_t lda,
@@ -151,6 +168,47 @@ gptq2d_status gptq2d_round(gptq2d_factors_t f, gptq2d_dtype dt, const void* X, i
 /* Synchronises `stream` and returns NONFINITE, OVERFLOW or TIMEOUT if the
  * last gptq2d_round that used `workspace` met one, OK otherwise. */
 gptq2d_status gptq2d_round_check(gptq2d_factors_t f, const void* workspace, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Batched rounding: many independent problems (the layers of a model, Sec. 6)
+ * in common launches. Stage k of every problem runs in one launch, so small
+ * problems, which occupy a few compute units each, share the device instead
+ * of running one after another.
+ * ------------------------------------------------------------------------- */
+
+/* Bytes of device workspace gptq2d_round_batched needs for the handles
+ * f[0 .. count-1] (a host array; a handle may appear more than once). 0 if
+ * count < 1, f is NULL or a handle is NULL. */
+size_t gptq2d_round_batched_workspace_size(int count, const gptq2d_factors_t* f);
+
+/* Enqueues the rounding of `count` problems, problem p exactly as
+ * gptq2d_round(f[p], dt, X[p], ldx[p], Z[p], ldz[p], Y[p], ldy[p], ...) would
+ * round it (the same kernels on the same data: identical Z, Y and objective).
+ *   f, X, ldx, Z, ldz: host arrays of `count` entries; X[p] and Z[p] are device
+ *       pointers (m_p x n_p, as for gptq2d_round); every problem has type dt.
+ *   Y, ldy: host arrays of `count` entries, or both NULL (no corrected values);
+ *       an entry Y[p] may be NULL.
+ *   objective: NULL, or a device array of `count` doubles (problem p's
+ *       objective in objective[p]).
+ *   workspace: device memory of at least gptq2d_round_batched_workspace_size
+ *       bytes for the same handles, 256-byte aligned, owned by the caller.
+ *       Calls that overlap need distinct workspaces and outputs; the host
+ *       arrays may be reused as soon as the call returns.
+ * 1 <= count; handles may repeat (problems that share their bases). Errors:
+ * INVALID_ARG, WORKSPACE, HIP. A non-finite X or an int32 overflow in any
+ * problem is recorded in the workspace and reported by
+ * gptq2d_round_batched_check. */
+gptq2d_status gptq2d_round_batched(int count, const gptq2d_factors_t* f, gptq2d_dtype dt,
+                                   const void* const* X, const int64_t* ldx, int32_t* const* Z,
+                                   const int64_t* ldz, void* const* Y, const int64_t* ldy,
+                                   double* objective, void* workspace, size_t ws_bytes,
+                                   void* stream);
+
+/* Synchronises `stream` and returns NONFINITE, OVERFLOW or TIMEOUT (in that
+ * order of precedence) if any problem of the last gptq2d_round_batched that
+ * used `workspace` met one, OK otherwise. The flags are the batch's, not a
+ * problem's: to find the problem, round it on its own. */
+gptq2d_status gptq2d_round_batched_check(const void* workspace, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Diagnostics

@@ -59,11 +59,16 @@ def load():
         "gptq2d_factor_compute": (i32, [vp, i32, vp, i64, vp, i64, vp]),
         "gptq2d_factor_check": (i32, [vp, vp]),
         "gptq2d_factor": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, ctypes.POINTER(vp)]),
+        "gptq2d_factor_batched": (i32, [i32, vp, i32, vp, vp, vp, vp, vp]),
+        "gptq2d_factor_batched_check": (i32, [i32, vp, vp]),
         "gptq2d_factors_export": (i32, [vp, vp, i64, vp, i64, vp, vp, vp]),
         "gptq2d_factors_import": (i32, [vp, vp, i64, vp, i64, vp, vp, vp]),
         "gptq2d_round_workspace_size": (sz, [vp]),
         "gptq2d_round": (i32, [vp, i32, vp, i64, vp, i64, vp, i64, vp, vp, sz, vp]),
         "gptq2d_round_check": (i32, [vp, vp, vp]),
+        "gptq2d_round_batched_workspace_size": (sz, [i32, vp]),
+        "gptq2d_round_batched": (i32, [i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "gptq2d_round_batched_check": (i32, [vp, vp]),
         "gptq2d_status_string": (ctypes.c_char_p, [i32]),
         "gptq2d_last_error": (ctypes.c_char_p, []),
         "gptq2d_version": (i32, []),
@@ -165,6 +170,30 @@ def gptq2d_factor_check(h: int, stream=None) -> None:
     _check(load().gptq2d_factor_check(ctypes.c_void_p(h), _stream(stream)), "gptq2d_factor_check")
 
 
+def gptq2d_factor_batched(handles, As, Bs, stream=None, shapes=None) -> None:
+    """Factorisations of len(handles) problems side by side (distinct handles)."""
+    count = len(handles)
+    if count == 0 or len(As) != count or len(Bs) != count:
+        raise ValueError("one A and one B per handle")
+    dt = _dt(As[0])
+    ap, al, bp, bl = [], [], [], []
+    for p, h in enumerate(handles):
+        m, n = shapes[p] if shapes is not None else gptq2d_factors_shape(h)
+        if _dt(As[p]) != dt or _dt(Bs[p]) != dt:
+            raise TypeError("every A and B of a batch must have the same dtype")
+        a, la = _mat(As[p], m, m, f"A[{p}]")
+        b, lb = _mat(Bs[p], n, n, f"B[{p}]")
+        ap.append(a.value); al.append(la); bp.append(b.value); bl.append(lb)
+    VP, I64 = ctypes.c_void_p * count, ctypes.c_int64 * count
+    _check(load().gptq2d_factor_batched(count, _handles(handles), dt, VP(*ap), I64(*al), VP(*bp), I64(*bl),
+                                        _stream(stream)), "gptq2d_factor_batched")
+
+
+def gptq2d_factor_batched_check(handles, stream=None) -> None:
+    _check(load().gptq2d_factor_batched_check(len(handles), _handles(handles), _stream(stream)),
+           "gptq2d_factor_batched_check")
+
+
 def gptq2d_factor(A: torch.Tensor, B: torch.Tensor, stream=None) -> int:
     if A.dtype != B.dtype:
         raise TypeError("A and B must share a dtype")
@@ -229,6 +258,62 @@ def gptq2d_round(h: int, X: torch.Tensor, Z: torch.Tensor, Y, objective, workspa
 def gptq2d_round_check(h: int, workspace: torch.Tensor, stream=None) -> None:
     _check(load().gptq2d_round_check(ctypes.c_void_p(h), _ptr(workspace), _stream(stream)),
            "gptq2d_round_check")
+
+
+def _handles(handles):
+    arr = (ctypes.c_void_p * len(handles))(*[int(h) for h in handles])
+    return arr
+
+
+def gptq2d_round_batched_workspace_size(handles) -> int:
+    return int(load().gptq2d_round_batched_workspace_size(len(handles), _handles(handles)))
+
+
+def gptq2d_round_batched(handles, Xs, Zs, Ys, objective, workspace: torch.Tensor, stream=None,
+                         shapes=None) -> None:
+    """Problems p = 0 .. len(handles)-1 in common launches; Ys may be None (or
+    hold None entries); objective None or a float64 device tensor of
+    len(handles) entries."""
+    count = len(handles)
+    if not (len(Xs) == len(Zs) == count) or (Ys is not None and len(Ys) != count):
+        raise ValueError("one X, Z (and Y) per handle")
+    if count == 0:
+        raise ValueError("empty batch")
+    dt = _dt(Xs[0])
+    xp, xl, zp, zl, yp, yl = [], [], [], [], [], []
+    for p, h in enumerate(handles):
+        m, n = shapes[p] if shapes is not None else gptq2d_factors_shape(h)
+        if _dt(Xs[p]) != dt:
+            raise TypeError("every X of a batch must have the same dtype")
+        a, la = _mat(Xs[p], m, n, f"X[{p}]")
+        if Zs[p].dtype != torch.int32:
+            raise TypeError("Z must be int32")
+        b, lb = _mat(Zs[p], m, n, f"Z[{p}]")
+        xp.append(a.value); xl.append(la); zp.append(b.value); zl.append(lb)
+        if Ys is not None:
+            if Ys[p] is None:
+                yp.append(None); yl.append(n)
+            else:
+                if Ys[p].dtype != Xs[p].dtype:
+                    raise TypeError("Y must have X's dtype")
+                c, lc = _mat(Ys[p], m, n, f"Y[{p}]")
+                yp.append(c.value); yl.append(lc)
+    if objective is not None and (objective.dtype != torch.float64 or not objective.is_cuda
+                                  or objective.numel() < count or not objective.is_contiguous()):
+        raise TypeError("objective must be a contiguous float64 device tensor of count entries")
+    VP, I64 = ctypes.c_void_p * count, ctypes.c_int64 * count
+    X_a, ldx_a, Z_a, ldz_a = VP(*xp), I64(*xl), VP(*zp), I64(*zl)
+    Y_a = VP(*yp) if Ys is not None else None
+    ldy_a = I64(*yl) if Ys is not None else None
+    _check(load().gptq2d_round_batched(count, _handles(handles), dt, X_a, ldx_a, Z_a, ldz_a, Y_a, ldy_a,
+                                       _ptr(objective), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _stream(stream)),
+           "gptq2d_round_batched")
+
+
+def gptq2d_round_batched_check(workspace: torch.Tensor, stream=None) -> None:
+    _check(load().gptq2d_round_batched_check(_ptr(workspace), _stream(stream)),
+           "gptq2d_round_batched_check")
 
 
 def gptq2d_stage_timing(h: int, enable: bool) -> None:
@@ -320,3 +405,29 @@ def round_matrix(f: Factors, X: torch.Tensor, want_y: bool = True, workspace=Non
     if check:
         gptq2d_round_check(f.handle, ws, stream)
     return Z, Y, obj
+
+
+def round_batched(factors, Xs, want_y: bool = True, workspace=None, check=True, stream=None):
+    """Round problem p = X[p] with factors[p] (a Factors may repeat), all in
+    common launches. Returns lists of Z, Y (or None) and the objectives as one
+    float64 device tensor."""
+    handles = [f.handle for f in factors]
+    dev = Xs[0].device
+    Zs = [torch.empty((f.m, f.n), dtype=torch.int32, device=dev) for f in factors]
+    Ys = [torch.empty((f.m, f.n), dtype=X.dtype, device=dev) for f, X in zip(factors, Xs)] if want_y else None
+    obj = torch.empty(len(factors), dtype=torch.float64, device=dev)
+    ws = workspace if workspace is not None else torch.empty(
+        gptq2d_round_batched_workspace_size(handles), dtype=torch.uint8, device=dev)
+    gptq2d_round_batched(handles, Xs, Zs, Ys, obj, ws, stream, shapes=[(f.m, f.n) for f in factors])
+    if check:
+        gptq2d_round_batched_check(ws, stream)
+    return Zs, Ys, obj
+
+
+def factor_batched(factors, As, Bs, check=True, stream=None):
+    """Compute the factors of every Factors in ``factors`` (distinct) from its
+    bases As[p], Bs[p], side by side."""
+    handles = [f.handle for f in factors]
+    gptq2d_factor_batched(handles, As, Bs, stream, shapes=[(f.m, f.n) for f in factors])
+    if check:
+        gptq2d_factor_batched_check(handles, stream)

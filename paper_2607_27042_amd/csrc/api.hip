@@ -38,8 +38,10 @@ static void free_all(Factors* f) {
   for (hipEvent_t ev : f->stage_ev) (void)hipEventDestroy(ev);
   f->stage_ev.clear();
   if (f->aux) (void)hipStreamDestroy(f->aux);
-  f->ev_near = f->ev_far = nullptr;
-  f->aux = nullptr;
+  if (f->ev_own) (void)hipEventDestroy(f->ev_own);
+  if (f->own) (void)hipStreamDestroy(f->own);
+  f->ev_near = f->ev_far = f->ev_own = nullptr;
+  f->aux = f->own = nullptr;
   free_schedule(f->sched);
 }
 
@@ -183,6 +185,59 @@ gptq2d_status gptq2d_factor_check(gptq2d_factors_t f, void* stream) {
   return GPTQ2D_OK;
 }
 
+gptq2d_status gptq2d_factor_batched(int count, const gptq2d_factors_t* f, gptq2d_dtype dt,
+                                    const void* const* A, const int64_t* lda, const void* const* B,
+                                    const int64_t* ldb, void* stream) {
+  if (count < 1) return fail(GPTQ2D_ERR_INVALID_ARG, "count must be at least 1");
+  if (!f || !A || !lda || !B || !ldb) return fail(GPTQ2D_ERR_INVALID_ARG, "an argument array is NULL");
+  if (dt != GPTQ2D_F32 && dt != GPTQ2D_F64) return fail(GPTQ2D_ERR_INVALID_ARG, "bad dtype");
+  for (int p = 0; p < count; ++p) {
+    if (!f[p]) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+    if (!A[p] || !B[p]) return fail(GPTQ2D_ERR_INVALID_ARG, "A or B is NULL");
+    if (lda[p] < f[p]->m || ldb[p] < f[p]->n)
+      return fail(GPTQ2D_ERR_INVALID_ARG, "leading dimension too small");
+    for (int q = 0; q < p; ++q)
+      if (f[q] == f[p]) return fail(GPTQ2D_ERR_INVALID_ARG, "a handle appears twice");
+    gptq2d_status st = check_device(f[p]);
+    if (st != GPTQ2D_OK) return st;
+  }
+  for (int p = 0; p < count; ++p) {
+    Factors* h = f[p];
+    if (!h->own) {
+      hipError_t e = hipStreamCreateWithFlags(&h->own, hipStreamNonBlocking);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_own, hipEventDisableTiming);
+      if (e != hipSuccess) return hip_fail(e, "stream / event creation");
+    }
+  }
+  hipStream_t s = (hipStream_t)stream;
+  hipEvent_t start = nullptr;
+  hipError_t e = hipEventCreateWithFlags(&start, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventRecord(start, s);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  gptq2d_status st = GPTQ2D_OK;
+  for (int p = 0; p < count && st == GPTQ2D_OK; ++p) {
+    Factors* h = f[p];
+    e = hipStreamWaitEvent(h->own, start, 0);
+    if (e != hipSuccess) { st = hip_fail(e, "hipStreamWaitEvent"); break; }
+    st = launch_factor(*h, dt, A[p], lda[p], B[p], ldb[p], h->own);
+    if (st != GPTQ2D_OK) break;
+    e = hipEventRecord(h->ev_own, h->own);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, h->ev_own, 0);
+    if (e != hipSuccess) st = hip_fail(e, "hipEventRecord");
+  }
+  (void)hipEventDestroy(start);  // released once the recorded work is done
+  return st;
+}
+
+gptq2d_status gptq2d_factor_batched_check(int count, const gptq2d_factors_t* f, void* stream) {
+  if (count < 1 || !f) return fail(GPTQ2D_ERR_INVALID_ARG, "empty batch");
+  for (int p = 0; p < count; ++p) {
+    gptq2d_status st = gptq2d_factor_check(f[p], stream);
+    if (st != GPTQ2D_OK) return st;
+  }
+  return GPTQ2D_OK;
+}
+
 gptq2d_status gptq2d_factor(int m, int n, gptq2d_dtype dt, const void* A, int64_t lda,
                             const void* B, int64_t ldb, void* stream, gptq2d_factors_t* out) {
   if (!out) return fail(GPTQ2D_ERR_INVALID_ARG, "out is NULL");
@@ -243,6 +298,53 @@ gptq2d_status gptq2d_round(gptq2d_factors_t f, gptq2d_dtype dt, const void* X, i
 
 gptq2d_status gptq2d_round_check(gptq2d_factors_t f, const void* workspace, void* stream) {
   if (!f || !workspace) return fail(GPTQ2D_ERR_INVALID_ARG, "handle or workspace is NULL");
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  int flags = 0;
+  e = hipMemcpy(&flags, workspace, sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+  if (flags & FLAG_NONFINITE) return fail(GPTQ2D_ERR_NONFINITE, "X held a NaN or an infinity");
+  if (flags & FLAG_OVERFLOW) return fail(GPTQ2D_ERR_OVERFLOW, "a rounded value does not fit in int32");
+  if (flags & FLAG_TIMEOUT) return fail(GPTQ2D_ERR_TIMEOUT, "a wave waited too long for its neighbour");
+  return GPTQ2D_OK;
+}
+
+size_t gptq2d_round_batched_workspace_size(int count, const gptq2d_factors_t* f) {
+  if (count < 1 || !f) return 0;
+  for (int p = 0; p < count; ++p)
+    if (!f[p]) return 0;
+  return batched_workspace_bytes(count, (const Factors* const*)f);
+}
+
+gptq2d_status gptq2d_round_batched(int count, const gptq2d_factors_t* f, gptq2d_dtype dt,
+                                   const void* const* X, const int64_t* ldx, int32_t* const* Z,
+                                   const int64_t* ldz, void* const* Y, const int64_t* ldy,
+                                   double* objective, void* workspace, size_t ws_bytes,
+                                   void* stream) {
+  if (count < 1) return fail(GPTQ2D_ERR_INVALID_ARG, "count must be at least 1");
+  if (!f || !X || !ldx || !Z || !ldz) return fail(GPTQ2D_ERR_INVALID_ARG, "an argument array is NULL");
+  if ((Y == nullptr) != (ldy == nullptr)) return fail(GPTQ2D_ERR_INVALID_ARG, "Y and ldy must both be given or both NULL");
+  if (dt != GPTQ2D_F32 && dt != GPTQ2D_F64) return fail(GPTQ2D_ERR_INVALID_ARG, "bad dtype");
+  for (int p = 0; p < count; ++p) {
+    if (!f[p]) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+    if (!X[p] || !Z[p]) return fail(GPTQ2D_ERR_INVALID_ARG, "X or Z is NULL");
+    if (ldx[p] < f[p]->n || ldz[p] < f[p]->n || (Y && Y[p] && ldy[p] < f[p]->n))
+      return fail(GPTQ2D_ERR_INVALID_ARG, "leading dimension too small");
+    gptq2d_status st = check_device(f[p]);
+    if (st != GPTQ2D_OK) return st;
+  }
+  const Factors* const* fs = (const Factors* const*)f;
+  if (!workspace || ws_bytes < batched_workspace_bytes(count, fs))
+    return fail(GPTQ2D_ERR_WORKSPACE,
+                "workspace missing or smaller than gptq2d_round_batched_workspace_size()");
+  if (((uintptr_t)workspace) % 256 != 0)
+    return fail(GPTQ2D_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return launch_round_batched(count, fs, dt, X, ldx, Z, ldz, Y, ldy, objective, workspace,
+                              (hipStream_t)stream);
+}
+
+gptq2d_status gptq2d_round_batched_check(const void* workspace, void* stream) {
+  if (!workspace) return fail(GPTQ2D_ERR_INVALID_ARG, "workspace is NULL");
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   int flags = 0;

@@ -23,6 +23,7 @@ struct Schedule {
   std::vector<int> bin_offset;   // per stage: first bin (size stages + 1)
   int4* d_tasks = nullptr;       // all tasks, grouped by stage, then by bin
   int4* d_bins = nullptr;        // {first task in the stage, counts by shape}, grouped by stage
+  int4* d_stage = nullptr;       // per stage: {offset, bin_offset, bins, 0} (batched rounding)
   size_t ntasks = 0;
 };
 
@@ -50,6 +51,10 @@ struct Factors {
   // trailing update runs there, next to the following group's panels
   hipStream_t aux = nullptr;
   hipEvent_t ev_near = nullptr, ev_far = nullptr;
+  // stream of this handle's factorisation inside a batched call (created on
+  // first use) and the event that marks its end
+  hipStream_t own = nullptr;
+  hipEvent_t ev_own = nullptr;
   Schedule sched;
   // launch timing of the sweep's stage kernel (diagnostics): while enabled,
   // every stage launch records its start and end time stamps into a pair of
@@ -98,5 +103,13 @@ void free_schedule(Schedule& s);
 gptq2d_status launch_round(const Factors& f, gptq2d_dtype dt, const void* X, int64_t ldx,
                            int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,
                            const Workspace& ws, hipStream_t s);
+
+// batched rounding: `count` problems, one workspace region each, in common
+// stage launches (workspace layout in sweep.hip)
+size_t batched_workspace_bytes(int count, const Factors* const* f);
+gptq2d_status launch_round_batched(int count, const Factors* const* f, gptq2d_dtype dt,
+                                   const void* const* X, const int64_t* ldx, int32_t* const* Z,
+                                   const int64_t* ldz, void* const* Y, const int64_t* ldy,
+                                   double* objective, void* workspace, hipStream_t s);
 
 }  // namespace g2d

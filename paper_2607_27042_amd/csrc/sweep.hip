@@ -25,6 +25,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <cstring>
 #include <functional>
 #include <queue>
 #include <vector>
@@ -60,6 +61,9 @@ struct StageArgs {
   const int4* tasks;  // this launch's deliveries, grouped by bin
   const int4* bins;   // this launch's bins (one work group each)
   int stage, ilo, nsweep;
+  // batched rounding: the problem's per-stage table {first task, first bin,
+  // bins, 0}; tasks and bins then point at the problem's whole plan
+  const int4* stab;
 };
 
 constexpr int SS = 16;       // sub-tile edge of the in-tile sweep
@@ -718,6 +722,77 @@ __global__ __launch_bounds__(NT) void k_stage(StageArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Batched rounding: independent problems (each with its own factors, X, Z, Y
+// and workspace region) share the stage launches. Launch k holds the stage-k
+// work groups of every problem that has a stage k: problem p owns the blocks
+// off[p] .. off[p+1]-1 and runs them exactly as k_stage would, so the merged
+// launch has the work of all problems in flight at once (small problems
+// occupy a few compute units each). Problem p's StageArgs (stage fields
+// unset) live in a device table.
+constexpr int BATCH_MAX = 512;  // problems per launch (block offsets travel as kernel arguments)
+struct BatchLaunch {
+  const StageArgs* desc;
+  int count, stage;
+  int off[BATCH_MAX + 1];
+};
+
+template <typename T>
+__global__ __launch_bounds__(NT) void k_stage_batch(BatchLaunch bl) {
+  __shared__ StageSmem sm;
+  const int b = blockIdx.x;
+  // the last p with off[p] <= b (problems without a stage k own no block)
+  int lo = 0, hi = bl.count - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (bl.off[mid] <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  StageArgs a = bl.desc[lo];
+  const int k = bl.stage, lb = b - bl.off[lo];
+  const int4 st = a.stab[k];
+  a.stage = k;
+  a.ilo = max(0, k - (a.NT - 1));
+  a.nsweep = min(k, a.MT - 1) - a.ilo + 1;
+  a.tasks = a.tasks ? a.tasks + st.x : nullptr;
+  a.bins = a.bins ? a.bins + st.y : nullptr;
+  if (lb < a.nsweep) {
+    const int I = a.ilo + lb;
+    run_sweep<T>(a, I, k - I, sm.s);
+  } else {
+    run_bin(a, a.bins[lb - a.nsweep], sm.t);
+  }
+}
+
+// Stream-ordered upload of up to PUT_WORDS 8-byte words passed as kernel
+// arguments (no host buffer has to outlive the call).
+constexpr int PUT_WORDS = 384;
+struct PutArgs {
+  uint64_t* dst;
+  int n;
+  uint64_t w[PUT_WORDS];
+};
+__global__ void k_put(PutArgs p) {
+  for (int i = threadIdx.x; i < p.n; i += blockDim.x) p.dst[i] = p.w[i];
+}
+
+// Objective of every problem of a batch: block p sums problem p's per-tile
+// partials in a fixed order.
+__global__ __launch_bounds__(NT) void k_obj_reduce_batch(const StageArgs* desc, double* out) {
+  __shared__ double red[NT];
+  const StageArgs& a = desc[blockIdx.x];
+  const int count = a.MT * a.NT;
+  double s = 0.0;
+  for (int i = threadIdx.x; i < count; i += NT) s += a.objp[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double tot = 0.0;
+    for (int i = 0; i < NT; ++i) tot += red[i];
+    out[blockIdx.x] = tot;
+  }
+}
+
 __global__ __launch_bounds__(NT) void k_obj_reduce(const double* part, int count, double* out) {
   __shared__ double red[NT];
   double s = 0.0;
@@ -972,8 +1047,10 @@ gptq2d_status pack_bins(int MT, int NTt, int units, std::vector<int4>& all,
 void free_schedule(Schedule& sc) {
   if (sc.d_tasks) (void)hipFree(sc.d_tasks);
   if (sc.d_bins) (void)hipFree(sc.d_bins);
+  if (sc.d_stage) (void)hipFree(sc.d_stage);
   sc.d_tasks = nullptr;
   sc.d_bins = nullptr;
+  sc.d_stage = nullptr;
 }
 
 gptq2d_status build_schedule(Factors& f, int g) {
@@ -1000,6 +1077,15 @@ gptq2d_status build_schedule(Factors& f, int g) {
     e = hipMemcpy(f.sched.d_bins, bins.data(), bins.size() * sizeof(int4), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "schedule upload");
   }
+  {
+    const int S = f.MT + f.NT - 1;
+    std::vector<int4> stab(S);
+    for (int k = 0; k < S; ++k) stab[k] = int4{off[k], boff[k], boff[k + 1] - boff[k], 0};
+    hipError_t e = hipMalloc(&f.sched.d_stage, S * sizeof(int4));
+    if (e != hipSuccess) return hip_fail(e, "schedule allocation");
+    e = hipMemcpy(f.sched.d_stage, stab.data(), S * sizeof(int4), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "schedule upload");
+  }
   f.sched.g = g;
   f.sched.stages = f.MT + f.NT - 1;
   f.sched.offset = off;
@@ -1009,10 +1095,9 @@ gptq2d_status build_schedule(Factors& f, int g) {
 }
 
 template <typename T>
-static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, int32_t* Z,
-                                 int64_t ldz, void* Y, int64_t ldy, double* objective,
-                                 const Workspace& ws, hipStream_t s) {
-  StageArgs a;
+static StageArgs stage_args(const Factors& f, const void* X, int64_t ldx, int32_t* Z, int64_t ldz,
+                            void* Y, int64_t ldy, const Workspace& ws) {
+  StageArgs a{};
   a.m = f.m;
   a.n = f.n;
   a.mp = f.mp;
@@ -1049,6 +1134,20 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
   a.C = ws.C;
   a.objp = ws.objp;
   a.flags = ws.flags;
+  return a;
+}
+
+// work groups of stage k of a problem: the tile sweeps beside the delivery bins
+static int stage_blocks(const Factors& f, int k) {
+  const int ilo = std::max(0, k - (f.NT - 1)), ihi = std::min(k, f.MT - 1);
+  return (ihi - ilo + 1) + (f.sched.bin_offset[k + 1] - f.sched.bin_offset[k]);
+}
+
+template <typename T>
+static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, int32_t* Z,
+                                 int64_t ldz, void* Y, int64_t ldy, double* objective,
+                                 const Workspace& ws, hipStream_t s) {
+  StageArgs a = stage_args<T>(f, X, ldx, Z, ldz, Y, ldy, ws);
   hipLaunchKernelGGL(k_zero_flags, dim3(1), dim3(64), 0, s, ws.flags);
   const Schedule& S = f.sched;
   for (int k = 0; k < S.stages; ++k) {
@@ -1087,6 +1186,80 @@ gptq2d_status launch_round(const Factors& f, gptq2d_dtype dt, const void* X, int
                            const Workspace& ws, hipStream_t s) {
   if (dt == GPTQ2D_F32) return round_typed<float>(f, X, ldx, Z, ldz, Y, ldy, objective, ws, s);
   return round_typed<double>(f, X, ldx, Z, ldz, Y, ldy, objective, ws, s);
+}
+
+// Workspace of a batch: the batch's error flags (256 bytes), the problems'
+// StageArgs table, then one gptq2d_round workspace region per problem.
+static size_t batch_table_bytes(int count) { return align256((size_t)count * sizeof(StageArgs)); }
+
+size_t batched_workspace_bytes(int count, const Factors* const* f) {
+  size_t b = 256 + batch_table_bytes(count);
+  for (int p = 0; p < count; ++p) b += align256(workspace_bytes(*f[p]));
+  return b;
+}
+
+template <typename T>
+static gptq2d_status round_batched_typed(int count, const Factors* const* f, const void* const* X,
+                                         const int64_t* ldx, int32_t* const* Z, const int64_t* ldz,
+                                         void* const* Y, const int64_t* ldy, double* objective,
+                                         void* workspace, hipStream_t s) {
+  static_assert(sizeof(StageArgs) % sizeof(uint64_t) == 0, "StageArgs is uploaded in 8-byte words");
+  char* base = (char*)workspace;
+  int* flags = (int*)base;
+  StageArgs* desc = (StageArgs*)(base + 256);
+  char* region = base + 256 + batch_table_bytes(count);
+  std::vector<StageArgs> h(count);
+  for (int p = 0; p < count; ++p) {
+    const Workspace ws = workspace_carve(*f[p], region);
+    region += align256(workspace_bytes(*f[p]));
+    h[p] = stage_args<T>(*f[p], X[p], ldx[p], Z[p], ldz[p], Y ? Y[p] : nullptr, Y ? ldy[p] : 0, ws);
+    h[p].flags = flags;
+    h[p].tasks = f[p]->sched.d_tasks;
+    h[p].bins = f[p]->sched.d_bins;
+    h[p].stab = f[p]->sched.d_stage;
+  }
+  hipLaunchKernelGGL(k_zero_flags, dim3(1), dim3(64), 0, s, flags);
+  // the table, in kernel-argument sized pieces
+  const uint64_t* words = reinterpret_cast<const uint64_t*>(h.data());
+  const size_t nwords = (size_t)count * sizeof(StageArgs) / sizeof(uint64_t);
+  for (size_t w0 = 0; w0 < nwords; w0 += PUT_WORDS) {
+    PutArgs pa;
+    pa.dst = reinterpret_cast<uint64_t*>(desc) + w0;
+    pa.n = (int)std::min<size_t>(PUT_WORDS, nwords - w0);
+    std::memcpy(pa.w, words + w0, pa.n * sizeof(uint64_t));
+    hipLaunchKernelGGL(k_put, dim3(1), dim3(NT), 0, s, pa);
+  }
+  for (int g0 = 0; g0 < count; g0 += BATCH_MAX) {
+    const int cnt = std::min(BATCH_MAX, count - g0);
+    int smax = 0;
+    for (int q = 0; q < cnt; ++q) smax = std::max(smax, f[g0 + q]->sched.stages);
+    BatchLaunch bl;
+    bl.desc = desc + g0;
+    bl.count = cnt;
+    for (int k = 0; k < smax; ++k) {
+      int tot = 0;
+      for (int q = 0; q < cnt; ++q) {
+        bl.off[q] = tot;
+        if (k < f[g0 + q]->sched.stages) tot += stage_blocks(*f[g0 + q], k);
+      }
+      bl.off[cnt] = tot;
+      bl.stage = k;
+      hipLaunchKernelGGL(k_stage_batch<T>, dim3(tot), dim3(NT), 0, s, bl);
+    }
+  }
+  if (objective) hipLaunchKernelGGL(k_obj_reduce_batch, dim3(count), dim3(NT), 0, s, desc, objective);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "batched sweep launch");
+  return GPTQ2D_OK;
+}
+
+gptq2d_status launch_round_batched(int count, const Factors* const* f, gptq2d_dtype dt,
+                                   const void* const* X, const int64_t* ldx, int32_t* const* Z,
+                                   const int64_t* ldz, void* const* Y, const int64_t* ldy,
+                                   double* objective, void* workspace, hipStream_t s) {
+  if (dt == GPTQ2D_F32)
+    return round_batched_typed<float>(count, f, X, ldx, Z, ldz, Y, ldy, objective, workspace, s);
+  return round_batched_typed<double>(count, f, X, ldx, Z, ldz, Y, ldy, objective, workspace, s);
 }
 
 }  // namespace g2d

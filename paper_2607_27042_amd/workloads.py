@@ -137,8 +137,12 @@ def _basis_c5(d, rng):
 _BASIS = {1: _basis_c1, 2: _basis_c2, 3: _basis_c3, 4: _basis_c4, 5: _basis_c5}
 
 
-def _x(k, m, n):
-    rng = np.random.default_rng([k, 0])
+def _seed(k, role, layer):
+    return [k, role] if layer == 0 else [k, role, layer]
+
+
+def _x(k, m, n, layer=0):
+    rng = np.random.default_rng(_seed(k, 0, layer))
     if k == 1:
         return 4.0 * rng.standard_normal((m, n))
     if k == 2:
@@ -170,17 +174,20 @@ def _cached(tag, fn):
     return v
 
 
-def make_config(k: int, dtype: str | None = None) -> Problem:
-    """The synthetic problem of config ``k`` (1..5) in run dtype ``dtype``."""
+def make_config(k: int, dtype: str | None = None, layer: int = 0) -> Problem:
+    """The synthetic problem of config ``k`` (1..5) in run dtype ``dtype``.
+    ``layer`` > 0 draws another problem from the same recipe (its own X and
+    bases, as the layers of one model), for batched runs."""
     m, n, dts = CONFIGS[k]
     dt = dtype or dts[0]
     if dt not in dts:
         raise ValueError(f"config {k} is defined for {dts}, not {dt}")
     npdt = _np_dtype(dt)
-    X = _cached(f"c{k}_X", lambda: _x(k, m, n))
-    A = _cached(f"c{k}_A", lambda: _BASIS[k](m, np.random.default_rng([k, 1])))
-    B = _cached(f"c{k}_B", lambda: _BASIS[k](n, np.random.default_rng([k, 2])))
-    name = f"c{k}_{m}x{n}_{dt}"
+    sfx = "" if layer == 0 else f"_l{layer}"
+    X = _cached(f"c{k}_X{sfx}", lambda: _x(k, m, n, layer))
+    A = _cached(f"c{k}_A{sfx}", lambda: _BASIS[k](m, np.random.default_rng(_seed(k, 1, layer))))
+    B = _cached(f"c{k}_B{sfx}", lambda: _BASIS[k](n, np.random.default_rng(_seed(k, 2, layer))))
+    name = f"c{k}_{m}x{n}_{dt}{sfx}"
     return Problem(name, np.ascontiguousarray(X.astype(npdt)),
                    np.ascontiguousarray(A.astype(npdt)), np.ascontiguousarray(B.astype(npdt)), dt)
 

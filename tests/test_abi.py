@@ -42,6 +42,17 @@ def test_null_handle_is_rejected(lib):
     assert lib.gptq2d_stage_timing(null, 1) == -1
     assert lib.gptq2d_stage_time(null, None, None) == -1
     assert lib.gptq2d_factors_set_order(null, 1) == -1
+    assert lib.gptq2d_round_batched_workspace_size(0, None) == 0
+    assert lib.gptq2d_round_batched_workspace_size(2, None) == 0
+    nulls = (ctypes.c_void_p * 2)(None, None)
+    assert lib.gptq2d_round_batched_workspace_size(2, nulls) == 0
+    assert lib.gptq2d_round_batched(0, None, 0, None, None, None, None, None, None, None, None, 0, None) == -1
+    assert lib.gptq2d_round_batched(2, nulls, 0, nulls, None, nulls, None, None, None, None, None, 0,
+                                    None) == -1
+    assert lib.gptq2d_round_batched_check(None, None) == -1
+    assert lib.gptq2d_factor_batched(0, None, 0, None, None, None, None, None) == -1
+    assert lib.gptq2d_factor_batched(2, nulls, 0, nulls, None, nulls, None, None) == -1
+    assert lib.gptq2d_factor_batched_check(0, None, None) == -1
     out = ctypes.c_void_p()
     assert lib.gptq2d_factors_create(0, 5, ctypes.byref(out)) == -1
     assert lib.gptq2d_factors_create(5, 70000, ctypes.byref(out)) == -1

@@ -1,0 +1,201 @@
+"""Batched rounding through the C ABI: problems of different shapes, orders
+and factor handles in common stage launches. Every problem must come out
+bit-identical to its own gptq2d_round (the same kernels on the same data),
+and that single-problem path is judged against the oracle here as well."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_27042_amd import binding, workloads as wl
+
+import parity as pr
+
+pytestmark = pytest.mark.gpu
+
+
+def _single(f, X):
+    Z, Y, obj = binding.round_matrix(f, X)
+    return Z.cpu().numpy(), Y.cpu().numpy(), float(obj.cpu()[0])
+
+
+def _check_batch(factors, Xs, probs=None):
+    Zs, Ys, obj = binding.round_batched(factors, Xs)
+    torch.cuda.synchronize()
+    objs = obj.cpu().numpy()
+    for p, (f, X) in enumerate(zip(factors, Xs)):
+        Z1, Y1, o1 = _single(f, X)
+        assert np.array_equal(Zs[p].cpu().numpy(), Z1), f"problem {p}: Z differs from the single call"
+        assert np.array_equal(Ys[p].cpu().numpy(), Y1), f"problem {p}: Y differs from the single call"
+        assert objs[p] == o1, f"problem {p}: objective {objs[p]!r} vs {o1!r}"
+        if probs is not None and probs[p] is not None:
+            prob, rev = probs[p]
+            X64, A, B = prob.widened()
+            tau = pr.TAU[prob.dtype]
+            if rev:
+                Zo, Yo, c, hard = oracle.round_reverse(X64, A, B, hint=Z1, tau=tau)
+            else:
+                L, lamL, U, lamU = oracle.factors(A, B)
+                Zo, Yo, c, hard = oracle.round_nested(X64, L, U, hint=Z1, tau=tau)
+            pr.assert_replay_pass(prob, c, hard, prob.m * prob.n)
+            pr.assert_objective(prob, objs[p], oracle.objective(X64, Zo, A, B))
+    return Zs, Ys, objs
+
+
+def test_mixed_batch_f64():
+    """Shapes from one tile to ragged multi-tile ones, one problem in reverse
+    order, and one handle used by two problems (shared bases, different X)."""
+    shapes = [(5, 7), (130, 200), (64, 64), (300, 257), (1, 100), (200, 130)]
+    probs, factors, Xs = [], [], []
+    for i, (m, n) in enumerate(shapes):
+        p = wl.random_problem(m, n, 20 + i, "f64", "wishart")
+        rev = i == 3
+        f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B), reverse=rev)
+        probs.append((p, rev)); factors.append(f); Xs.append(pr.to_dev(p.X))
+    # a second X on the handle of the 130 x 200 problem
+    p2 = wl.random_problem(130, 200, 40, "f64", "wishart")
+    X2 = pr.to_dev(p2.X)
+    factors.append(factors[1]); Xs.append(X2); probs.append(None)
+    print(f"[batch] mixed f64, {len(factors)} problems", flush=True)
+    _check_batch(factors, Xs, probs)
+    for f in factors:
+        f.close()
+
+
+def test_batch_of_small_configs_f32():
+    """Eight 512 x 384 problems (fp32 inputs), four handles shared by two X each."""
+    factors, Xs, probs = [], [], []
+    hs = []
+    for i in range(4):
+        p = wl.random_problem(512, 384, 60 + i, "f32", "wishart")
+        hs.append((p, binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B))))
+    for i in range(8):
+        p, f = hs[i % 4]
+        X = p.X if i < 4 else (wl.random_problem(512, 384, 70 + i, "f32", "wishart").X)
+        factors.append(f); Xs.append(pr.to_dev(X))
+        probs.append((p, False) if i < 4 else None)
+    print("[batch] 8 x 512x384 f32", flush=True)
+    _check_batch(factors, Xs, probs)
+    for _, f in hs:
+        f.close()
+
+
+def test_batch_larger_than_one_launch():
+    """More problems than one launch's block table holds: the batch runs in
+    consecutive groups of launches."""
+    pa = wl.random_problem(5, 7, 80, "f64", "wishart")
+    pb = wl.random_problem(70, 3, 81, "f64", "general")
+    fa = binding.Factors.from_bases(pr.to_dev(pa.A), pr.to_dev(pa.B))
+    fb = binding.Factors.from_bases(pr.to_dev(pb.A), pr.to_dev(pb.B))
+    rng = np.random.default_rng(82)
+    factors, Xs = [], []
+    for i in range(530):
+        f, p = (fa, pa) if i % 3 else (fb, pb)
+        factors.append(f)
+        Xs.append(pr.to_dev(4.0 * rng.standard_normal((p.m, p.n))))
+    print("[batch] 530 tiny problems", flush=True)
+    Zs, Ys, obj = binding.round_batched(factors, Xs)
+    torch.cuda.synchronize()
+    objs = obj.cpu().numpy()
+    for p in (0, 1, 2, 511, 512, 513, 529):
+        Z1, Y1, o1 = _single(factors[p], Xs[p])
+        assert np.array_equal(Zs[p].cpu().numpy(), Z1), p
+        assert np.array_equal(Ys[p].cpu().numpy(), Y1), p
+        assert objs[p] == o1, p
+    fa.close()
+    fb.close()
+
+
+def test_batch_without_y_and_objective():
+    p = wl.random_problem(100, 90, 90, "f64", "wishart")
+    f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B))
+    X = pr.to_dev(p.X)
+    Z = torch.empty((100, 90), dtype=torch.int32, device="cuda")
+    ws = torch.empty(binding.gptq2d_round_batched_workspace_size([f.handle]), dtype=torch.uint8,
+                     device="cuda")
+    binding.gptq2d_round_batched([f.handle], [X], [Z], None, None, ws)
+    binding.gptq2d_round_batched_check(ws)
+    Z1, _, _ = _single(f, X)
+    assert np.array_equal(Z.cpu().numpy(), Z1)
+    f.close()
+
+
+def test_batch_errors():
+    p = wl.random_problem(64, 64, 91, "f64", "wishart")
+    f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B))
+    X = pr.to_dev(p.X)
+    bad = X.clone()
+    bad[3, 5] = float("nan")
+    size = binding.gptq2d_round_batched_workspace_size([f.handle, f.handle])
+    assert size > 2 * binding.gptq2d_round_workspace_size(f.handle)
+    ws = torch.empty(size, dtype=torch.uint8, device="cuda")
+    Zs = [torch.empty((64, 64), dtype=torch.int32, device="cuda") for _ in range(2)]
+    with pytest.raises(binding.Gptq2dError) as e:
+        binding.gptq2d_round_batched([f.handle, f.handle], [X, X], Zs, None, None, ws[: size - 256])
+    assert e.value.status == -6  # GPTQ2D_ERR_WORKSPACE
+    binding.gptq2d_round_batched([f.handle, f.handle], [X, bad], Zs, None, None, ws)
+    with pytest.raises(binding.Gptq2dError) as e:
+        binding.gptq2d_round_batched_check(ws)
+    assert e.value.status == -3  # GPTQ2D_ERR_NONFINITE
+    # the same workspace is clean again on the next call
+    binding.gptq2d_round_batched([f.handle, f.handle], [X, X], Zs, None, None, ws)
+    binding.gptq2d_round_batched_check(ws)
+    f.close()
+
+
+def _export(f):
+    L, U, lamL, lamU = f.export()
+    torch.cuda.synchronize()
+    return [t.cpu().numpy() for t in (L, U, lamL, lamU)]
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_factor_batched_matches_single(dtype):
+    """Factorisations side by side: each handle's factors are bit-identical to
+    its own gptq2d_factor_compute and close to the oracle's; then the whole
+    batched path (factor + round) is replayed by the oracle."""
+    shapes = [(5, 7), (130, 200), (384, 128), (256, 320), (64, 64), (1, 1)]
+    probs = [wl.random_problem(m, n, 30 + i, dtype, "wishart") for i, (m, n) in enumerate(shapes)]
+    fs = [binding.Factors(p.m, p.n, reverse=(i == 2)) for i, p in enumerate(probs)]
+    As = [pr.to_dev(p.A) for p in probs]
+    Bs = [pr.to_dev(p.B) for p in probs]
+    print(f"[batch] factor {len(fs)} problems {dtype}", flush=True)
+    binding.factor_batched(fs, As, Bs)
+    for i, (p, f) in enumerate(zip(probs, fs)):
+        got = _export(f)
+        single = binding.Factors.from_bases(As[i], Bs[i], reverse=(i == 2))
+        ref = _export(single)
+        single.close()
+        for g, r in zip(got, ref):
+            assert np.array_equal(g, r), f"problem {i}: factors differ from the single call"
+        X, A, B = p.widened()
+        if i == 2:
+            _, A, B = oracle.reverse_problem(X, A, B)
+        L, lamL, U, lamU = oracle.factors(A, B)
+        err = np.abs(got[0] - L).max() / max(1.0, np.abs(L).max())
+        assert err <= 1e-10, (i, err)
+        np.testing.assert_allclose(got[2], lamL, rtol=1e-10)
+        np.testing.assert_allclose(got[3], lamU, rtol=1e-10)
+    Xs = [pr.to_dev(p.X) for p in probs]
+    _check_batch(fs, Xs, [(p, i == 2) for i, p in enumerate(probs)])
+    for f in fs:
+        f.close()
+
+
+def test_factor_batched_errors():
+    pa = wl.random_problem(70, 40, 95, "f64", "wishart")
+    fa = binding.Factors(70, 40)
+    fb = binding.Factors(70, 40)
+    A, B = pr.to_dev(pa.A), pr.to_dev(pa.B)
+    with pytest.raises(binding.Gptq2dError) as e:
+        binding.factor_batched([fa, fa], [A, A], [B, B])
+    assert e.value.status == -1  # a handle twice
+    sing = A.clone()
+    sing[:, 7] = 0.0
+    binding.factor_batched([fa, fb], [A, sing], [B, B], check=False)
+    with pytest.raises(binding.Gptq2dError) as e:
+        binding.gptq2d_factor_batched_check([fa.handle, fb.handle])
+    assert e.value.status == -2  # singular basis
+    binding.gptq2d_factor_batched_check([fa.handle])
+    fa.close()
+    fb.close()
