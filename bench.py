@@ -161,12 +161,13 @@ def run_batch(args, dev):
     Ys = [torch.empty((m, n), dtype=Xs[0].dtype, device=dev) for _ in range(N)]
     obj = torch.empty(N, dtype=torch.float64, device=dev)
     ws = torch.empty(binding.gptq2d_round_batched_workspace_size(handles), dtype=torch.uint8, device=dev)
+    fws = torch.empty(binding.gptq2d_factor_batched_workspace_size(N), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        binding.gptq2d_factor_batched(handles, As, Bs, stream, shapes=shapes)
+        binding.gptq2d_factor_batched(handles, As, Bs, fws, stream, shapes=shapes)
         if ev is not None:
             ev[1].record(stream)
         binding.gptq2d_round_batched(handles, Xs, Zs, Ys, obj, ws, stream, shapes=shapes)

@@ -104,18 +104,28 @@ gptq2d_status gptq2d_factor_compute(gptq2d_factors_t f, gptq2d_dtype dt, const v
  * met a non-positive or non-finite pivot, OK otherwise. */
 gptq2d_status gptq2d_factor_check(gptq2d_factors_t f, void* stream);
 
+/* Bytes of device workspace gptq2d_factor_batched needs for `count` problems
+ * (0 if count < 1). */
+size_t gptq2d_factor_batched_workspace_size(int count);
+
 /* Enqueues the factorisation of `count` problems at once: problem p as
  * gptq2d_factor_compute(f[p], dt, A[p], lda[p], B[p], ldb[p], stream) would,
- * with the same result. f, A, lda, B, ldb are host arrays (A[p], B[p] device
- * pointers); a handle may appear only once. The problems run side by side
- * (each handle on a stream of its own, created on its first batched use and
- * ordered after the work already on `stream`); `stream` waits for all of
- * them. Small problems, whose factorisation is a chain of short launches,
- * overlap instead of queueing behind one another. Allocates no device
- * memory; does not synchronise. Errors: INVALID_ARG, HIP. */
+ * with the same bits. f, A, lda, B, ldb are host arrays (A[p], B[p] device
+ * pointers); a handle may appear only once. Problems of one shape (m, n) are
+ * factorised in common launches: every step of the factorisation runs for
+ * all of them in one launch, so small problems, whose factorisation is a
+ * chain of short launches, share each launch instead of queueing. Groups of
+ * different shapes run side by side, each on a stream of the group's first
+ * handle (created on its first batched use), ordered after the work already
+ * on `stream`; `stream` then waits for all of them. workspace: device memory
+ * of at least gptq2d_factor_batched_workspace_size(count) bytes, 256-byte
+ * aligned, owned by the caller (the batch's argument table); overlapping
+ * calls need distinct workspaces. Allocates no device memory; does not
+ * synchronise. Errors: INVALID_ARG, WORKSPACE, HIP. */
 gptq2d_status gptq2d_factor_batched(int count, const gptq2d_factors_t* f, gptq2d_dtype dt,
                                     const void* const* A, const int64_t* lda, const void* const* B,
-                                    const int64_t* ldb, void* stream);
+                                    const int64_t* ldb, void* workspace, size_t ws_bytes,
+                                    void* stream);
 
 /* Synchronises `stream` and returns SINGULAR if the last factorisation of any
  * of the handles f[0 .. count-1] met a non-positive or non-finite pivot. */

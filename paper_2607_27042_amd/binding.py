@@ -59,7 +59,8 @@ def load():
         "gptq2d_factor_compute": (i32, [vp, i32, vp, i64, vp, i64, vp]),
         "gptq2d_factor_check": (i32, [vp, vp]),
         "gptq2d_factor": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, ctypes.POINTER(vp)]),
-        "gptq2d_factor_batched": (i32, [i32, vp, i32, vp, vp, vp, vp, vp]),
+        "gptq2d_factor_batched_workspace_size": (sz, [i32]),
+        "gptq2d_factor_batched": (i32, [i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
         "gptq2d_factor_batched_check": (i32, [i32, vp, vp]),
         "gptq2d_factors_export": (i32, [vp, vp, i64, vp, i64, vp, vp, vp]),
         "gptq2d_factors_import": (i32, [vp, vp, i64, vp, i64, vp, vp, vp]),
@@ -170,8 +171,13 @@ def gptq2d_factor_check(h: int, stream=None) -> None:
     _check(load().gptq2d_factor_check(ctypes.c_void_p(h), _stream(stream)), "gptq2d_factor_check")
 
 
-def gptq2d_factor_batched(handles, As, Bs, stream=None, shapes=None) -> None:
-    """Factorisations of len(handles) problems side by side (distinct handles)."""
+def gptq2d_factor_batched_workspace_size(count: int) -> int:
+    return int(load().gptq2d_factor_batched_workspace_size(count))
+
+
+def gptq2d_factor_batched(handles, As, Bs, workspace: torch.Tensor, stream=None, shapes=None) -> None:
+    """Factorisations of len(handles) problems (distinct handles) in common
+    launches per shape."""
     count = len(handles)
     if count == 0 or len(As) != count or len(Bs) != count:
         raise ValueError("one A and one B per handle")
@@ -186,6 +192,7 @@ def gptq2d_factor_batched(handles, As, Bs, stream=None, shapes=None) -> None:
         ap.append(a.value); al.append(la); bp.append(b.value); bl.append(lb)
     VP, I64 = ctypes.c_void_p * count, ctypes.c_int64 * count
     _check(load().gptq2d_factor_batched(count, _handles(handles), dt, VP(*ap), I64(*al), VP(*bp), I64(*bl),
+                                        _ptr(workspace), workspace.numel() * workspace.element_size(),
                                         _stream(stream)), "gptq2d_factor_batched")
 
 
@@ -424,10 +431,12 @@ def round_batched(factors, Xs, want_y: bool = True, workspace=None, check=True, 
     return Zs, Ys, obj
 
 
-def factor_batched(factors, As, Bs, check=True, stream=None):
+def factor_batched(factors, As, Bs, check=True, stream=None, workspace=None):
     """Compute the factors of every Factors in ``factors`` (distinct) from its
-    bases As[p], Bs[p], side by side."""
+    bases As[p], Bs[p], in common launches per shape."""
     handles = [f.handle for f in factors]
-    gptq2d_factor_batched(handles, As, Bs, stream, shapes=[(f.m, f.n) for f in factors])
+    ws = workspace if workspace is not None else torch.empty(
+        gptq2d_factor_batched_workspace_size(len(handles)), dtype=torch.uint8, device=As[0].device)
+    gptq2d_factor_batched(handles, As, Bs, ws, stream, shapes=[(f.m, f.n) for f in factors])
     if check:
         gptq2d_factor_batched_check(handles, stream)

@@ -185,9 +185,14 @@ gptq2d_status gptq2d_factor_check(gptq2d_factors_t f, void* stream) {
   return GPTQ2D_OK;
 }
 
+size_t gptq2d_factor_batched_workspace_size(int count) {
+  return count < 1 ? 0 : (factor_batch_table_bytes(count) + 255) / 256 * 256;
+}
+
 gptq2d_status gptq2d_factor_batched(int count, const gptq2d_factors_t* f, gptq2d_dtype dt,
                                     const void* const* A, const int64_t* lda, const void* const* B,
-                                    const int64_t* ldb, void* stream) {
+                                    const int64_t* ldb, void* workspace, size_t ws_bytes,
+                                    void* stream) {
   if (count < 1) return fail(GPTQ2D_ERR_INVALID_ARG, "count must be at least 1");
   if (!f || !A || !lda || !B || !ldb) return fail(GPTQ2D_ERR_INVALID_ARG, "an argument array is NULL");
   if (dt != GPTQ2D_F32 && dt != GPTQ2D_F64) return fail(GPTQ2D_ERR_INVALID_ARG, "bad dtype");
@@ -201,8 +206,38 @@ gptq2d_status gptq2d_factor_batched(int count, const gptq2d_factors_t* f, gptq2d
     gptq2d_status st = check_device(f[p]);
     if (st != GPTQ2D_OK) return st;
   }
+  if (!workspace || ws_bytes < gptq2d_factor_batched_workspace_size(count))
+    return fail(GPTQ2D_ERR_WORKSPACE,
+                "workspace missing or smaller than gptq2d_factor_batched_workspace_size()");
+  if (((uintptr_t)workspace) % 256 != 0)
+    return fail(GPTQ2D_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  // groups of problems of one shape (in order of first appearance), each
+  // factorised in common launches, the groups side by side
+  std::vector<int> order;
+  std::vector<std::pair<int, int>> groups;  // (first position in order, size)
+  std::vector<char> taken(count, 0);
   for (int p = 0; p < count; ++p) {
-    Factors* h = f[p];
+    if (taken[p]) continue;
+    const int first = (int)order.size();
+    for (int q = p; q < count; ++q)
+      if (!taken[q] && f[q]->m == f[p]->m && f[q]->n == f[p]->n) {
+        taken[q] = 1;
+        order.push_back(q);
+      }
+    groups.emplace_back(first, (int)order.size() - first);
+  }
+  std::vector<Factors*> gf(count);
+  std::vector<const void*> gA(count), gB(count);
+  std::vector<int64_t> glda(count), gldb(count);
+  for (int i = 0; i < count; ++i) {
+    gf[i] = f[order[i]];
+    gA[i] = A[order[i]];
+    gB[i] = B[order[i]];
+    glda[i] = lda[order[i]];
+    gldb[i] = ldb[order[i]];
+  }
+  for (const auto& g : groups) {
+    Factors* h = gf[g.first];
     if (!h->own) {
       hipError_t e = hipStreamCreateWithFlags(&h->own, hipStreamNonBlocking);
       if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_own, hipEventDisableTiming);
@@ -215,15 +250,26 @@ gptq2d_status gptq2d_factor_batched(int count, const gptq2d_factors_t* f, gptq2d
   if (e == hipSuccess) e = hipEventRecord(start, s);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
   gptq2d_status st = GPTQ2D_OK;
-  for (int p = 0; p < count && st == GPTQ2D_OK; ++p) {
-    Factors* h = f[p];
+  for (const auto& g : groups) {
+    const int i0 = g.first, cnt = g.second;
+    Factors* h = gf[i0];
     e = hipStreamWaitEvent(h->own, start, 0);
-    if (e != hipSuccess) { st = hip_fail(e, "hipStreamWaitEvent"); break; }
-    st = launch_factor(*h, dt, A[p], lda[p], B[p], ldb[p], h->own);
+    if (e != hipSuccess) {
+      st = hip_fail(e, "hipStreamWaitEvent");
+      break;
+    }
+    if (cnt == 1)
+      st = launch_factor(*h, dt, gA[i0], glda[i0], gB[i0], gldb[i0], h->own);
+    else
+      st = launch_factor_batched(cnt, &gf[i0], dt, &gA[i0], &glda[i0], &gB[i0], &gldb[i0],
+                                 (char*)workspace + factor_batch_table_bytes(i0), h->own);
     if (st != GPTQ2D_OK) break;
     e = hipEventRecord(h->ev_own, h->own);
     if (e == hipSuccess) e = hipStreamWaitEvent(s, h->ev_own, 0);
-    if (e != hipSuccess) st = hip_fail(e, "hipEventRecord");
+    if (e != hipSuccess) {
+      st = hip_fail(e, "hipEventRecord");
+      break;
+    }
   }
   (void)hipEventDestroy(start);  // released once the recorded work is done
   return st;

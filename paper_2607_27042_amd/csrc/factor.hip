@@ -18,6 +18,9 @@
 #include <math.h>
 
 #include <algorithm>
+#include <cstring>
+#include <type_traits>
+#include <vector>
 
 #include "device.hpp"
 #include "internal.hpp"
@@ -40,6 +43,35 @@ struct FacArgs {
   int* flags;
   int rev;  // reverse order: the index-reversed problem (A P, P B), so no reversal below
 };
+
+// Batched factorisation: problems of one shape in common launches. Problem p
+// owns the blocks p per .. p per + per - 1 of a launch (per = the grid of a
+// single problem's launch) and takes its FacArgs and inputs from a device
+// table; every block then does exactly what it does in a single problem's
+// launch, so the results are the same bits.
+struct FacProb {
+  FacArgs f;
+  const void* A;
+  const void* B;
+  int64_t lda, ldb;
+  double* gpart;
+};
+struct BatchCtx {
+  const FacProb* tab;  // unused by single-problem launches
+  int per;
+};
+template <bool BAT>
+__device__ __forceinline__ const FacProb* bat_prob(const BatchCtx& bc) {
+  return BAT ? bc.tab + blockIdx.x / bc.per : nullptr;
+}
+template <bool BAT>
+__device__ __forceinline__ int bat_block(const BatchCtx& bc) {
+  return BAT ? (int)(blockIdx.x % bc.per) : (int)blockIdx.x;
+}
+template <bool BAT>
+__device__ __forceinline__ int bat_grid(const BatchCtx& bc) {
+  return BAT ? bc.per : (int)gridDim.x;
+}
 
 // Lower-triangle enumeration of tile pairs: b -> (i, j) with i >= j.
 __device__ __forceinline__ void tri_index(int b, int& i, int& j) {
@@ -149,17 +181,23 @@ __device__ void gram_tile(const Side& sd, const T* S, int64_t ld, int bp, int bq
 
 // Sides in a Gram launch: side 0 if bit 0 of `sides` is set, side 1 if bit
 // 1 is; the grid holds the lower tiles of the first, then of the second.
-template <typename T>
-__global__ __launch_bounds__(NT) void k_gram(FacArgs f, const T* A, int64_t lda, const T* B,
-                                             int64_t ldb, int sides) {
+template <typename T, bool BAT>
+__global__ __launch_bounds__(NT) void k_gram(FacArgs f0, const T* A0, int64_t lda0, const T* B0,
+                                             int64_t ldb0, int sides, BatchCtx bc) {
   __shared__ Stage64 st;
+  const FacProb* pb = bat_prob<BAT>(bc);
+  const FacArgs& f = BAT ? pb->f : f0;
+  const T* A = BAT ? (const T*)pb->A : A0;
+  const T* B = BAT ? (const T*)pb->B : B0;
+  const int64_t lda = BAT ? pb->lda : lda0, ldb = BAT ? pb->ldb : ldb0;
+  const int bid = bat_block<BAT>(bc);
   const int t0 = (sides & 1) ? f.s[0].nb * (f.s[0].nb + 1) / 2 : 0;
   int bp, bq;
-  if ((int)blockIdx.x < t0) {
-    tri_index(blockIdx.x, bp, bq);
+  if (bid < t0) {
+    tri_index(bid, bp, bq);
     gram_tile<T, 0>(f.s[0], A, lda, bp, bq, st, f.rev);
   } else {
-    tri_index(blockIdx.x - t0, bp, bq);
+    tri_index(bid - t0, bp, bq);
     gram_tile<T, 1>(f.s[1], B, ldb, bp, bq, st, f.rev);
   }
 }
@@ -190,12 +228,17 @@ struct GramChunk {
   double b[32][GA];   // rows 128 bq ..
 };
 
-template <typename T>
-__global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f, const T* A, int64_t lda, const T* B,
-                                                  int64_t ldb, int sides) {
+template <typename T, bool BAT>
+__global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f0, const T* A0, int64_t lda0, const T* B0,
+                                                  int64_t ldb0, int sides, BatchCtx bc) {
   __shared__ double tile[TB][TB + 1];
+  const FacProb* pb = bat_prob<BAT>(bc);
+  const FacArgs& f = BAT ? pb->f : f0;
+  const T* A = BAT ? (const T*)pb->A : A0;
+  const T* B = BAT ? (const T*)pb->B : B0;
+  const int64_t lda = BAT ? pb->lda : lda0, ldb = BAT ? pb->ldb : ldb0;
   const int n0 = (sides & 1) ? (f.s[0].d / TB) * (f.s[0].d / TB) : 0;
-  int b = blockIdx.x;
+  int b = bat_block<BAT>(bc);
   const int side = b < n0 ? 0 : 1;
   if (side == 1) b -= n0;
   const Side& sd = f.s[side];
@@ -355,16 +398,21 @@ __device__ __forceinline__ double* gram_slot(double* part, int slot, int h) {
   return part + ((int64_t)(2 * slot + h) << 14) + threadIdx.x;
 }
 
-__global__ __launch_bounds__(NT) void k_gram128(FacArgs f, GramPlan pl, double* part) {
+template <bool BAT>
+__global__ __launch_bounds__(NT) void k_gram128(FacArgs f0, GramPlan pl, double* part0, BatchCtx bc) {
   __shared__ GramChunk buf[2];
+  const FacProb* pb = bat_prob<BAT>(bc);
+  const FacArgs& f = BAT ? pb->f : f0;
+  double* part = BAT ? pb->gpart : part0;
+  const int bid = bat_block<BAT>(bc);
   // work groups are dealt round-robin to the eight L2 domains (XCDs): give
   // each domain a contiguous run of ranges, so that the tiles it runs at the
   // same time share their row panel (tri_index enumerates row by row)
   // (domain x holds the work groups i = x mod 8, q of them, and gets the
   // ranges from x q + min(x, r) on, with q, r the quotient and remainder by 8)
   const int q8 = pl.G / 8, r8 = pl.G % 8;
-  const int x = blockIdx.x % 8;
-  const int jr = x * q8 + min(x, r8) + (int)blockIdx.x / 8;
+  const int x = bid % 8;
+  const int jr = x * q8 + min(x, r8) + bid / 8;
   const int64_t hi = pl.lo(jr + 1);
   d4 acc[4][4];
   for (int64_t u = pl.lo(jr); u < hi;) {
@@ -394,8 +442,12 @@ __global__ __launch_bounds__(NT) void k_gram128(FacArgs f, GramPlan pl, double* 
 }
 
 // Tiles split between ranges jr and jr + 1: head + tail, stored as a finished tile.
-__global__ __launch_bounds__(NT) void k_gram_fix(FacArgs f, GramPlan pl, const double* part) {
-  const int jr = blockIdx.x;
+template <bool BAT>
+__global__ __launch_bounds__(NT) void k_gram_fix(FacArgs f0, GramPlan pl, const double* part0, BatchCtx bc) {
+  const FacProb* pb = bat_prob<BAT>(bc);
+  const FacArgs& f = BAT ? pb->f : f0;
+  const double* part = BAT ? pb->gpart : part0;
+  const int jr = bat_block<BAT>(bc);
   const int64_t u = pl.lo(jr + 1);
   int side, b, c;
   pl.at(u, side, b, c);
@@ -654,9 +706,11 @@ __device__ void diag_tile(const Side& sd, int kb, int* flags, DiagSmem& ds) {
   }
 }
 
-__global__ __launch_bounds__(NT) void k_diag(FacArgs f, int kb) {
+template <bool BAT>
+__global__ __launch_bounds__(NT) void k_diag(FacArgs f0, int kb, BatchCtx bc) {
   __shared__ DiagSmem ds;
-  const Side& sd = f.s[blockIdx.x];
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  const Side& sd = f.s[bat_block<BAT>(bc)];
   if (kb >= sd.nb) return;
   diag_tile(sd, kb, f.flags, ds);
 }
@@ -672,9 +726,11 @@ __device__ __forceinline__ int panel_count(const Side& sd, int kb) {
   return kb < sd.nb ? (sd.nb - kb - 1) + (kb + 1) : 0;
 }
 
-__global__ __launch_bounds__(NT) void k_panel(FacArgs f, int kb) {
+template <bool BAT>
+__global__ __launch_bounds__(NT) void k_panel(FacArgs f0, int kb, BatchCtx bc) {
   __shared__ Stage64 st;
-  int b = blockIdx.x;
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  int b = bat_block<BAT>(bc);
   const int n0 = panel_count(f.s[0], kb);
   const Side& sd = (b < n0) ? f.s[0] : f.s[1];
   if (b >= n0) b -= n0;
@@ -747,18 +803,20 @@ __device__ void gemm_blocks(Acc& acc, const double* pa, int64_t lda, int64_t sa_
   }
 }
 
-__global__ __launch_bounds__(NT) void k_update(FacArgs f, UpdRange r) {
+template <bool BAT>
+__global__ __launch_bounds__(NT) void k_update(FacArgs f0, UpdRange r, BatchCtx bc) {
   __shared__ union {
     Stage64 st[2];
     DiagSmem d;
   } sm;
   Stage64* st = sm.st;
-  int b = blockIdx.x;
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  int b = bat_block<BAT>(bc);
   int nq0, ns0;
   upd_counts(f.s[0], r, nq0, ns0);
   // the two sides' diagonal blocks (the first Q tile of each side) go to
   // the first two work groups: their factorisation is the longest chain
-  if (r.dg >= 0 && nq0 + ns0 > 1 && nq0 + ns0 < (int)gridDim.x) {
+  if (r.dg >= 0 && nq0 + ns0 > 1 && nq0 + ns0 < bat_grid<BAT>(bc)) {
     if (b == 1) b = nq0 + ns0;
     else if (b == nq0 + ns0) b = 1;
   }
@@ -981,10 +1039,13 @@ __device__ void update128_tile(const FacArgs& f, int g0, int g1, int g2, int b, 
 // ntile tiles over the grid, tile b by work group b mod gridDim.x: a grid
 // smaller than the device leaves compute units to the diagonal blocks and
 // panels that run beside it on the other stream
-__global__ __launch_bounds__(NT) void k_update128(FacArgs f, int g0, int g1, int g2, int ntile) {
+template <bool BAT>
+__global__ __launch_bounds__(NT) void k_update128(FacArgs f0, int g0, int g1, int g2, int ntile, BatchCtx bc) {
   __shared__ UpdChunk buf[2];
-  for (int b = blockIdx.x; b < ntile; b += gridDim.x) {
-    if (b != (int)blockIdx.x) __syncthreads();  // the staging buffers are reused
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  const int bid = bat_block<BAT>(bc), grid = bat_grid<BAT>(bc);
+  for (int b = bid; b < ntile; b += grid) {
+    if (b != bid) __syncthreads();  // the staging buffers are reused
     update128_tile(f, g0, g1, g2, b, buf);
   }
 }
@@ -998,14 +1059,17 @@ __global__ __launch_bounds__(NT) void k_update128(FacArgs f, int g0, int g1, int
 // triangle's tiles are written, and only they are ever read.
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(NT) void k_finalize(FacArgs f) {
+template <bool BAT>
+__global__ __launch_bounds__(NT) void k_finalize(FacArgs f0, BatchCtx bc) {
   __shared__ double S[TB][TB + 1];
   __shared__ double sc[TB];
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  const int bid = bat_block<BAT>(bc);
   const int t0 = f.s[0].nb * (f.s[0].nb + 1) / 2;
-  const int side = (int)blockIdx.x < t0 ? 0 : 1;
+  const int side = bid < t0 ? 0 : 1;
   const Side& sd = f.s[side];
   int bi, bj;
-  tri_index(side == 0 ? blockIdx.x : blockIdx.x - t0, bi, bj);  // bi >= bj
+  tri_index(side == 0 ? bid : bid - t0, bi, bj);  // bi >= bj
   const int d = sd.d, dp = sd.dp;
   const int rs = d - TB - bj * TB, cs = d - TB - bi * TB;
   const int t = threadIdx.x;
@@ -1036,6 +1100,42 @@ __global__ __launch_bounds__(NT) void k_finalize(FacArgs f) {
     const int i = bi * TB + t;
     sd.dout[i] = (i < d) ? sc[63 - t] * sc[63 - t] : 1.0;
   }
+}
+
+__global__ void k_zero_flags_batch(const FacProb* tab, int count) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p < count) tab[p].f.flags[0] = 0;
+}
+
+// Stream-ordered upload of up to PUT_WORDS 8-byte words that travel as
+// kernel arguments (no host buffer has to outlive the enqueueing call).
+constexpr int PUT_WORDS = 384;
+struct PutArgs {
+  uint64_t* dst;
+  int n;
+  uint64_t w[PUT_WORDS];
+};
+__global__ void k_put(PutArgs p) {
+  for (int i = threadIdx.x; i < p.n; i += blockDim.x) p.dst[i] = p.w[i];
+}
+
+static gptq2d_status check_launch(const char* what);
+
+gptq2d_status enqueue_upload(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  if (bytes % sizeof(uint64_t) != 0 || ((uintptr_t)dst) % sizeof(uint64_t) != 0) {
+    set_error("upload of a partial word");
+    return GPTQ2D_ERR_INVALID_ARG;
+  }
+  const uint64_t* words = static_cast<const uint64_t*>(src);
+  const size_t nwords = bytes / sizeof(uint64_t);
+  for (size_t w0 = 0; w0 < nwords; w0 += PUT_WORDS) {
+    PutArgs pa;
+    pa.dst = static_cast<uint64_t*>(dst) + w0;
+    pa.n = (int)std::min<size_t>(PUT_WORDS, nwords - w0);
+    std::memcpy(pa.w, words + w0, pa.n * sizeof(uint64_t));
+    hipLaunchKernelGGL(k_put, dim3(1), dim3(NT), 0, s, pa);
+  }
+  return check_launch("upload");
 }
 
 __global__ void k_zero_int(int* p, int n) {
@@ -1118,12 +1218,24 @@ static void h_far_counts(int nb, int g0, int g1, int g2, int& nq, int& ns) {
   ns = (nb2 - t0) * (g0 / 2);
 }
 
-gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t lda,
-                            const void* B, int64_t ldb, hipStream_t s) {
+// The factorisation of one problem (tab == nullptr: its inputs A, B), or of
+// `count` problems of f's shape whose FacArgs and inputs are in the device
+// table `tab` (A, B unused); f provides the shape, the second stream and the
+// events either way.
+static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq2d_dtype dt,
+                                 const void* A, int64_t lda, const void* B, int64_t ldb,
+                                 hipStream_t s) {
   FacArgs a = fac_args(f);
   const int nb0 = a.s[0].nb, nb1 = a.s[1].nb, nbmax = nb0 > nb1 ? nb0 : nb1;
   const int tri = nb0 * (nb0 + 1) / 2 + nb1 * (nb1 + 1) / 2;
-  hipLaunchKernelGGL(k_zero_int, dim3(1), dim3(64), 0, s, f.flags, 1);
+  // launch with `per` work groups per problem
+  auto go = [&](int per, hipStream_t st, auto&& launch) {
+    if (per <= 0) return;
+    if (!tab) launch(std::false_type{}, dim3(per), BatchCtx{nullptr, 0}, st);
+    else launch(std::true_type{}, dim3(per * count), BatchCtx{tab, per}, st);
+  };
+  if (!tab) hipLaunchKernelGGL(k_zero_int, dim3(1), dim3(64), 0, s, f.flags, 1);
+  else hipLaunchKernelGGL(k_zero_flags_batch, dim3((count + 63) / 64), dim3(64), 0, s, tab, count);
   // Gram: sides whose dimension is a multiple of 128 through the prepared
   // panel and 128 x 128 tiles, the others with 64 x 64 tiles straight from
   // the input
@@ -1139,27 +1251,42 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
     }
   }
   if (fast) {
-    if (dt == GPTQ2D_F32)
-      hipLaunchKernelGGL(k_gram_prep<float>, dim3(nprep), dim3(NT), 0, s, a, (const float*)A, lda,
-                         (const float*)B, ldb, fast);
-    else
-      hipLaunchKernelGGL(k_gram_prep<double>, dim3(nprep), dim3(NT), 0, s, a, (const double*)A,
-                         lda, (const double*)B, ldb, fast);
+    go(nprep, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+      constexpr bool BT = decltype(bat)::value;
+      if (dt == GPTQ2D_F32)
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram_prep<float, BT>), g, dim3(NT), 0, st, a,
+                           (const float*)A, lda, (const float*)B, ldb, fast, bc);
+      else
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram_prep<double, BT>), g, dim3(NT), 0, st, a,
+                           (const double*)A, lda, (const double*)B, ldb, fast, bc);
+    });
     const GramPlan pl = gram_plan(f.m, f.n, fast, f.cus);
-    hipLaunchKernelGGL(k_gram128, dim3(pl.G), dim3(NT), 0, s, a, pl, f.gpart);
-    if (pl.G > 1) hipLaunchKernelGGL(k_gram_fix, dim3(pl.G - 1), dim3(NT), 0, s, a, pl, (const double*)f.gpart);
+    go(pl.G, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+      constexpr bool BT = decltype(bat)::value;
+      hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram128<BT>), g, dim3(NT), 0, st, a, pl, f.gpart, bc);
+    });
+    go(pl.G - 1, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+      constexpr bool BT = decltype(bat)::value;
+      hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram_fix<BT>), g, dim3(NT), 0, st, a, pl,
+                         (const double*)f.gpart, bc);
+    });
   }
   if (slow) {
-    if (dt == GPTQ2D_F32)
-      hipLaunchKernelGGL(k_gram<float>, dim3(nslow), dim3(NT), 0, s, a, (const float*)A, lda,
-                         (const float*)B, ldb, slow);
-    else
-      hipLaunchKernelGGL(k_gram<double>, dim3(nslow), dim3(NT), 0, s, a, (const double*)A, lda,
-                         (const double*)B, ldb, slow);
+    go(nslow, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+      constexpr bool BT = decltype(bat)::value;
+      if (dt == GPTQ2D_F32)
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram<float, BT>), g, dim3(NT), 0, st, a, (const float*)A,
+                           lda, (const float*)B, ldb, slow, bc);
+      else
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram<double, BT>), g, dim3(NT), 0, st, a,
+                           (const double*)A, lda, (const double*)B, ldb, slow, bc);
+    });
   }
   auto update = [&](const UpdRange& r, hipStream_t st) {
-    const int nu = h_upd_count(nb0, r) + h_upd_count(nb1, r);
-    if (nu > 0) hipLaunchKernelGGL(k_update, dim3(nu), dim3(NT), 0, st, a, r);
+    go(h_upd_count(nb0, r) + h_upd_count(nb1, r), st, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t q) {
+      constexpr bool BT = decltype(bat)::value;
+      hipLaunchKernelGGL(HIP_KERNEL_NAME(k_update<BT>), g, dim3(NT), 0, q, a, r, bc);
+    });
   };
   // Groups of GROUP panels (an even count: the far part works on pairs of
   // block columns). Inside a group, before each panel, its column of Q and
@@ -1180,9 +1307,16 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
       // the diagonal block of every later panel is factored by the update
       // that completes it (the in-group update of the panel before, or the
       // group's near update for the next group's first panel)
-      if (kb == 0) hipLaunchKernelGGL(k_diag, dim3(2), dim3(NT), 0, s, a, kb);
-      const int np_ = h_panel_count(nb0, kb) + h_panel_count(nb1, kb);
-      if (np_ > 0) hipLaunchKernelGGL(k_panel, dim3(np_), dim3(NT), 0, s, a, kb);
+      if (kb == 0)
+        go(2, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+          constexpr bool BT = decltype(bat)::value;
+          hipLaunchKernelGGL(HIP_KERNEL_NAME(k_diag<BT>), g, dim3(NT), 0, st, a, kb, bc);
+        });
+      go(h_panel_count(nb0, kb) + h_panel_count(nb1, kb), s,
+         [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+           constexpr bool BT = decltype(bat)::value;
+           hipLaunchKernelGGL(HIP_KERNEL_NAME(k_panel<BT>), g, dim3(NT), 0, st, a, kb, bc);
+         });
       // left-looking inside the group: the next panel's column of Q and row
       // of S get all of the group's finished panels at once (the later
       // columns wait for their own turn)
@@ -1210,8 +1344,12 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
         // a far update of a few tiles per compute unit leaves 32 units to the
         // diagonal blocks and panels beside it (measured best at 4096); a
         // larger one is the longer of the two streams and takes every unit
-        const int grid = nfar > 4 * units ? nfar : std::max(1, std::min(nfar, units - 32));
-        hipLaunchKernelGGL(k_update128, dim3(grid), dim3(NT), 0, f.aux, a, g0, g1, g2, nfar);
+        // (a batch fills the device by itself: one tile per work group)
+        const int grid = tab || nfar > 4 * units ? nfar : std::max(1, std::min(nfar, units - 32));
+        go(grid, f.aux, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+          constexpr bool BT = decltype(bat)::value;
+          hipLaunchKernelGGL(HIP_KERNEL_NAME(k_update128<BT>), g, dim3(NT), 0, st, a, g0, g1, g2, nfar, bc);
+        });
       }
       update(UpdRange{g2, g2, g2, nbmax, g0, g1, g0, -1}, f.aux);
       he = hipEventRecord(f.ev_far, f.aux);
@@ -1223,8 +1361,36 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
     he = hipStreamWaitEvent(s, f.ev_far, 0);
     if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
   }
-  hipLaunchKernelGGL(k_finalize, dim3(tri), dim3(NT), 0, s, a);
+  go(tri, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+    constexpr bool BT = decltype(bat)::value;
+    hipLaunchKernelGGL(HIP_KERNEL_NAME(k_finalize<BT>), g, dim3(NT), 0, st, a, bc);
+  });
   return check_launch("factorisation launch");
+}
+
+gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t lda,
+                            const void* B, int64_t ldb, hipStream_t s) {
+  return factor_impl(f, nullptr, 0, dt, A, lda, B, ldb, s);
+}
+
+size_t factor_batch_table_bytes(int count) { return (size_t)count * sizeof(FacProb); }
+
+gptq2d_status launch_factor_batched(int count, Factors* const* fs, gptq2d_dtype dt,
+                                    const void* const* A, const int64_t* lda, const void* const* B,
+                                    const int64_t* ldb, void* table, hipStream_t s) {
+  static_assert(sizeof(FacProb) % sizeof(uint64_t) == 0, "the table is uploaded in 8-byte words");
+  std::vector<FacProb> h(count);
+  for (int p = 0; p < count; ++p) {
+    h[p].f = fac_args(*fs[p]);
+    h[p].A = A[p];
+    h[p].B = B[p];
+    h[p].lda = lda[p];
+    h[p].ldb = ldb[p];
+    h[p].gpart = fs[p]->gpart;
+  }
+  gptq2d_status st = enqueue_upload(table, h.data(), h.size() * sizeof(FacProb), s);
+  if (st != GPTQ2D_OK) return st;
+  return factor_impl(*fs[0], (const FacProb*)table, count, dt, nullptr, 0, nullptr, 0, s);
 }
 
 gptq2d_status launch_export(const Factors& f, double* L, int64_t ldl, double* U, int64_t ldu,

@@ -84,6 +84,16 @@ gptq2d_status hip_fail(hipError_t e, const char* what);
 // factorisation launches (enqueued on stream, no synchronisation)
 // doubles of scratch for the Gram tiles split between work groups
 size_t gram_part_doubles(int m, int n, int cus);
+// stream-ordered upload of host words into device memory (bytes and dst
+// multiples of 8; the host buffer may be reused on return)
+gptq2d_status enqueue_upload(void* dst, const void* src, size_t bytes, hipStream_t s);
+// batched factorisation of problems of one shape (fs[0]'s second stream and
+// events order it); `table` holds factor_batch_table_bytes(count) bytes of
+// device memory
+size_t factor_batch_table_bytes(int count);
+gptq2d_status launch_factor_batched(int count, Factors* const* fs, gptq2d_dtype dt,
+                                    const void* const* A, const int64_t* lda, const void* const* B,
+                                    const int64_t* ldb, void* table, hipStream_t s);
 gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t lda,
                             const void* B, int64_t ldb, hipStream_t s);
 gptq2d_status launch_export(const Factors& f, double* L, int64_t ldl, double* U, int64_t ldu,

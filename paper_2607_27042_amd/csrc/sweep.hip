@@ -764,18 +764,6 @@ __global__ __launch_bounds__(NT) void k_stage_batch(BatchLaunch bl) {
   }
 }
 
-// Stream-ordered upload of up to PUT_WORDS 8-byte words passed as kernel
-// arguments (no host buffer has to outlive the call).
-constexpr int PUT_WORDS = 384;
-struct PutArgs {
-  uint64_t* dst;
-  int n;
-  uint64_t w[PUT_WORDS];
-};
-__global__ void k_put(PutArgs p) {
-  for (int i = threadIdx.x; i < p.n; i += blockDim.x) p.dst[i] = p.w[i];
-}
-
 // Objective of every problem of a batch: block p sums problem p's per-tile
 // partials in a fixed order.
 __global__ __launch_bounds__(NT) void k_obj_reduce_batch(const StageArgs* desc, double* out) {
@@ -1203,7 +1191,7 @@ static gptq2d_status round_batched_typed(int count, const Factors* const* f, con
                                          const int64_t* ldx, int32_t* const* Z, const int64_t* ldz,
                                          void* const* Y, const int64_t* ldy, double* objective,
                                          void* workspace, hipStream_t s) {
-  static_assert(sizeof(StageArgs) % sizeof(uint64_t) == 0, "StageArgs is uploaded in 8-byte words");
+  static_assert(sizeof(StageArgs) % sizeof(uint64_t) == 0, "the table is uploaded in 8-byte words");
   char* base = (char*)workspace;
   int* flags = (int*)base;
   StageArgs* desc = (StageArgs*)(base + 256);
@@ -1219,16 +1207,8 @@ static gptq2d_status round_batched_typed(int count, const Factors* const* f, con
     h[p].stab = f[p]->sched.d_stage;
   }
   hipLaunchKernelGGL(k_zero_flags, dim3(1), dim3(64), 0, s, flags);
-  // the table, in kernel-argument sized pieces
-  const uint64_t* words = reinterpret_cast<const uint64_t*>(h.data());
-  const size_t nwords = (size_t)count * sizeof(StageArgs) / sizeof(uint64_t);
-  for (size_t w0 = 0; w0 < nwords; w0 += PUT_WORDS) {
-    PutArgs pa;
-    pa.dst = reinterpret_cast<uint64_t*>(desc) + w0;
-    pa.n = (int)std::min<size_t>(PUT_WORDS, nwords - w0);
-    std::memcpy(pa.w, words + w0, pa.n * sizeof(uint64_t));
-    hipLaunchKernelGGL(k_put, dim3(1), dim3(NT), 0, s, pa);
-  }
+  const gptq2d_status st = enqueue_upload(desc, h.data(), h.size() * sizeof(StageArgs), s);
+  if (st != GPTQ2D_OK) return st;
   for (int g0 = 0; g0 < count; g0 += BATCH_MAX) {
     const int cnt = std::min(BATCH_MAX, count - g0);
     int smax = 0;

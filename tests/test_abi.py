@@ -50,8 +50,10 @@ def test_null_handle_is_rejected(lib):
     assert lib.gptq2d_round_batched(2, nulls, 0, nulls, None, nulls, None, None, None, None, None, 0,
                                     None) == -1
     assert lib.gptq2d_round_batched_check(None, None) == -1
-    assert lib.gptq2d_factor_batched(0, None, 0, None, None, None, None, None) == -1
-    assert lib.gptq2d_factor_batched(2, nulls, 0, nulls, None, nulls, None, None) == -1
+    assert lib.gptq2d_factor_batched_workspace_size(0) == 0
+    assert lib.gptq2d_factor_batched_workspace_size(3) >= 256
+    assert lib.gptq2d_factor_batched(0, None, 0, None, None, None, None, None, 0, None) == -1
+    assert lib.gptq2d_factor_batched(2, nulls, 0, nulls, None, nulls, None, None, 0, None) == -1
     assert lib.gptq2d_factor_batched_check(0, None, None) == -1
     out = ctypes.c_void_p()
     assert lib.gptq2d_factors_create(0, 5, ctypes.byref(out)) == -1

@@ -149,35 +149,44 @@ def _export(f):
     return [t.cpu().numpy() for t in (L, U, lamL, lamU)]
 
 
+# repeated shapes go through the common launches: the 64-wide Gram path
+# (130 x 200), the 128-wide one (384 x 128), Gram tiles split between work
+# groups (640 x 384), several panel groups with the far update on the second
+# stream (600 x 520), single tiles; a lone shape takes the single-problem path
+BATCH_SHAPES = [(130, 200), (384, 128), (130, 200), (640, 384), (600, 520), (64, 64), (384, 128),
+                (5, 7), (640, 384), (130, 200), (600, 520), (64, 64), (1, 1), (1, 1)]
+
+
 @pytest.mark.parametrize("dtype", ["f64", "f32"])
 def test_factor_batched_matches_single(dtype):
-    """Factorisations side by side: each handle's factors are bit-identical to
-    its own gptq2d_factor_compute and close to the oracle's; then the whole
-    batched path (factor + round) is replayed by the oracle."""
-    shapes = [(5, 7), (130, 200), (384, 128), (256, 320), (64, 64), (1, 1)]
-    probs = [wl.random_problem(m, n, 30 + i, dtype, "wishart") for i, (m, n) in enumerate(shapes)]
-    fs = [binding.Factors(p.m, p.n, reverse=(i == 2)) for i, p in enumerate(probs)]
+    """Factorisations in common launches: each handle's factors are
+    bit-identical to its own gptq2d_factor_compute and close to the oracle's;
+    then the whole batched path (factor + round) is replayed by the oracle."""
+    probs = [wl.random_problem(m, n, 30 + i, dtype, "wishart") for i, (m, n) in enumerate(BATCH_SHAPES)]
+    rev = [i % 4 == 2 for i in range(len(probs))]
+    fs = [binding.Factors(p.m, p.n, reverse=rev[i]) for i, p in enumerate(probs)]
     As = [pr.to_dev(p.A) for p in probs]
     Bs = [pr.to_dev(p.B) for p in probs]
     print(f"[batch] factor {len(fs)} problems {dtype}", flush=True)
     binding.factor_batched(fs, As, Bs)
     for i, (p, f) in enumerate(zip(probs, fs)):
         got = _export(f)
-        single = binding.Factors.from_bases(As[i], Bs[i], reverse=(i == 2))
+        single = binding.Factors.from_bases(As[i], Bs[i], reverse=rev[i])
         ref = _export(single)
         single.close()
         for g, r in zip(got, ref):
-            assert np.array_equal(g, r), f"problem {i}: factors differ from the single call"
+            assert np.array_equal(g, r), f"problem {i} {p.m}x{p.n}: factors differ from the single call"
         X, A, B = p.widened()
-        if i == 2:
+        if rev[i]:
             _, A, B = oracle.reverse_problem(X, A, B)
         L, lamL, U, lamU = oracle.factors(A, B)
-        err = np.abs(got[0] - L).max() / max(1.0, np.abs(L).max())
+        err = max(np.abs(got[0] - L).max() / max(1.0, np.abs(L).max()),
+                  np.abs(got[1] - U).max() / max(1.0, np.abs(U).max()))
         assert err <= 1e-10, (i, err)
         np.testing.assert_allclose(got[2], lamL, rtol=1e-10)
         np.testing.assert_allclose(got[3], lamU, rtol=1e-10)
     Xs = [pr.to_dev(p.X) for p in probs]
-    _check_batch(fs, Xs, [(p, i == 2) for i, p in enumerate(probs)])
+    _check_batch(fs, Xs, [(p, rev[i]) for i, p in enumerate(probs)])
     for f in fs:
         f.close()
 
