@@ -148,6 +148,29 @@ def test_reverse_order(m, n, dtype):
         assert not np.array_equal(fwd["Z"], res["Z"])
 
 
+@pytest.mark.parametrize("m,n,dtype", [(130, 200, "f64"), (384, 256, "f32"), (700, 1000, "f32")])
+def test_transposed_problem_same_z(m, n, dtype):
+    """||A (Z - X) B|| = ||B^T (Z^T - X^T) A^T||, and the column-major sweep of
+    the transposed problem is the row-major order of the original, another
+    admissible order: by Theorem 1 the GPU's Z of (X^T, B^T, A^T) is the
+    transpose of its Z of (X, A, B), and the objectives agree."""
+    p = wl.random_problem(m, n, 17, dtype, "general")
+    print(f"[transpose] {m}x{n} {dtype}", flush=True)
+    res = pr.gpu_run(p)
+    pt = wl.Problem(p.name + "_T", np.ascontiguousarray(p.X.T), np.ascontiguousarray(p.B.T),
+                    np.ascontiguousarray(p.A.T), p.dtype)
+    rt = pr.gpu_run(pt)
+    mism = int((res["Z"] != rt["Z"].T).sum())
+    assert mism <= 1e-4 * m * n, mism
+    rel = abs(res["obj"] - rt["obj"]) / res["obj"]
+    assert rel <= pr.OBJ_RTOL[dtype], rel
+    # and the oracle agrees with the transposed run too
+    Xt, At, Bt = pt.widened()
+    L, lamL, U, lamU = oracle.factors(At, Bt)
+    Zo, Yo, c, hard = oracle.round_nested(Xt, L, U, hint=rt["Z"], tau=pr.TAU[dtype])
+    pr.assert_replay_pass(pt, c, hard, m * n)
+
+
 @pytest.mark.parametrize("kind", ["diag", "identity_right", "identity_left", "lower"])
 def test_special_bases(kind):
     p = wl.random_problem(97, 131, 6, "f64", kind)
