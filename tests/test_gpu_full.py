@@ -68,3 +68,54 @@ def test_full_size_config(k, dtype):
     D = res["Z"].astype(np.float64) - X
     obj_def = float(np.linalg.norm((A @ D) @ B) ** 2)
     pr.assert_objective(p, res["obj"], obj_def)
+
+
+def test_full_size_reverse_order_c3():
+    """Reverse order at 4096 x 4096: the GPU's Z reversed is the forward sweep
+    of the index-reversed problem (P X P, A P, P B), whose leading corner the
+    oracle replays with the GPU's factors (those of the reversed problem); the
+    objective by its definition in X's own indexing."""
+    import oracle
+    p = wl.make_config(3, "f32")
+    print(f"[full] {p.name} reverse order: GPU factor + sweep", flush=True)
+    res = pr.gpu_run(p, reverse=True)
+    X, A, B = p.widened()
+    Xr, Ar, Br = oracle.reverse_problem(X, A, B)
+    pr_rev = wl.Problem(p.name + "_rev", Xr.astype(np.float32), Ar.astype(np.float32),
+                        Br.astype(np.float32), p.dtype)
+    Zr = np.ascontiguousarray(res["Z"][::-1, ::-1])
+    Zo, Yo, c, hard = pr.replay(pr_rev, res["L"], res["U"], Zr, corner=(CORNER, CORNER))
+    pr.assert_replay_pass(pr_rev, c, hard, CORNER * CORNER)
+    assert _factor_residual(Ar, res["L"], res["lamL"], left=True) <= 1e-9
+    assert _factor_residual(Br, res["U"], res["lamU"], left=False) <= 1e-9
+    D = res["Z"].astype(np.float64) - X
+    pr.assert_objective(p, res["obj"], float(np.linalg.norm((A @ D) @ B) ** 2))
+
+
+def test_full_size_batched_equals_single():
+    """Two 4096 x 4096 problems (the c3 recipe, layers 0 and 1, their own bases)
+    through the batched factorisation and sweep: factors, Z, Y and objectives
+    bit-identical to each problem's single-problem calls."""
+    import torch
+
+    from paper_2607_27042_amd import binding
+    probs = [wl.make_config(3, "f32", layer=i) for i in range(2)]
+    As = [pr.to_dev(q.A) for q in probs]
+    Bs = [pr.to_dev(q.B) for q in probs]
+    Xs = [pr.to_dev(q.X) for q in probs]
+    print("[full] 2 x c3 batched", flush=True)
+    fs = [binding.Factors(q.m, q.n) for q in probs]
+    binding.factor_batched(fs, As, Bs)
+    Zs, Ys, obj = binding.round_batched(fs, Xs)
+    torch.cuda.synchronize()
+    for i in range(2):
+        single = binding.Factors.from_bases(As[i], Bs[i])
+        Z1, Y1, o1 = binding.round_matrix(single, Xs[i])
+        for a, b in zip(fs[i].export(), single.export()):
+            assert torch.equal(a, b), f"problem {i}: factors differ"
+        assert torch.equal(Zs[i], Z1), f"problem {i}: Z differs"
+        assert torch.equal(Ys[i], Y1), f"problem {i}: Y differs"
+        assert float(obj[i]) == float(o1[0]), f"problem {i}: objective differs"
+        single.close()
+    for f in fs:
+        f.close()
