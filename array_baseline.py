@@ -1,0 +1,109 @@
+"""The paper's own array-framework realisation of the sweep, as a comparison
+point for the HIP path (it is not part of that path and nothing in the
+library calls it).
+
+Blocked GPTQ-2D (Sec. 4.3, Algorithm 4) written with PyTorch tensor
+operations, on any device: blocks of w consecutive anti-diagonals; inside a
+block every anti-diagonal is rounded in parallel with the fold and both
+pushes clipped at the block's last anti-diagonal (Algorithm 3 restricted to
+the block); after the block, the down flush (the band of E through L, which
+also completes C = L E below the block) and the right flush (the band of C
+through U) reach every later entry as batched matrix-vector products over
+windows of w columns of L and w rows of U that shift with the receiving
+column or row. Indices are 0-based: anti-diagonal s holds the entries
+i + j = s, s = 0 .. m + n - 2.
+
+Ties of the rounding go to even (torch.round), as everywhere in this build.
+The factors are inputs: L unit lower (m x m) and U unit upper (n x n) of the
+inverse Grams, with L_ii = U_jj = 1.
+"""
+from __future__ import annotations
+
+import torch
+
+
+def _diag_rows(m: int, n: int, s: int, device):
+    lo, hi = max(0, s - n + 1), min(s, m - 1)
+    return torch.arange(lo, hi + 1, device=device)
+
+
+def blocked_sweep(X: torch.Tensor, L: torch.Tensor, U: torch.Tensor, w: int = 16,
+                  col_chunk: int | None = None):
+    """Z (rounded values, X's dtype), Y (corrected values) and E = Z - Y of
+    Algorithm 4 with block width w. col_chunk bounds the columns (rows) whose
+    flush windows are gathered at once (memory: col_chunk * max(m, n) * w
+    values)."""
+    m, n = X.shape
+    dev, dt = X.device, X.dtype
+    Y = X.clone()
+    C = torch.zeros_like(X)
+    E = torch.zeros_like(X)
+    Z = torch.zeros_like(X)
+    S = m + n - 1
+    chunk = col_chunk or max(1, (1 << 25) // (max(m, n) * w))
+    ar_w = torch.arange(w, device=dev)
+    # zero-padded factors so that every window of w columns (rows) exists
+    Lp = torch.zeros((m, m + 2 * w), dtype=dt, device=dev)
+    Lp[:, w:w + m] = L
+    Up = torch.zeros((n + 2 * w, n), dtype=dt, device=dev)
+    Up[w:w + n, :] = U
+    Ep = torch.zeros((m + 2 * w, n), dtype=dt, device=dev)  # E with w zero rows above and below
+    Cp = torch.zeros((m, n + 2 * w), dtype=dt, device=dev)  # C with w zero columns left and right
+    ii = torch.arange(m, device=dev)[:, None]
+    jj = torch.arange(n, device=dev)[None, :]
+    for s0 in range(0, S, w):
+        s1 = min(s0 + w - 1, S - 1)
+        # ---- inside the block: Algorithm 3 with the fold and pushes clipped at s1
+        for s in range(s0, s1 + 1):
+            I = _diag_rows(m, n, s, dev)
+            J = s - I
+            y = Y[I, J]
+            z = torch.round(y)
+            e = z - y
+            Z[I, J] = z
+            E[I, J] = e
+            D = s1 - s  # rows i .. i + D (columns j .. j + D) stay inside the block
+            R = I[:, None] + torch.arange(D + 1, device=dev)[None, :]
+            ok = R < m
+            Rc = torch.where(ok, R, torch.zeros_like(R))
+            M = torch.where(ok, L[Rc, I[:, None]] * e[:, None], torch.zeros((), dtype=dt, device=dev))
+            Jb = J[:, None].expand_as(R)
+            C.index_put_((Rc[ok], Jb[ok]), M[ok], accumulate=True)  # fold (L_ii = 1: C_ij gets E_ij)
+            if D > 0:
+                ok1 = ok[:, 1:]
+                Y.index_put_((Rc[:, 1:][ok1], Jb[:, 1:][ok1]), M[:, 1:][ok1], accumulate=True)  # push down
+                Q = J[:, None] + 1 + torch.arange(D, device=dev)[None, :]
+                okq = Q < n
+                Qc = torch.where(okq, Q, torch.zeros_like(Q))
+                cij = C[I, J]
+                V = cij[:, None] * U[J[:, None], Qc]
+                Ib = I[:, None].expand_as(Q)
+                Y.index_put_((Ib[okq], Qc[okq]), V[okq], accumulate=True)  # push right
+        if s1 == S - 1:
+            break
+        later = (ii + jj) > s1
+        # ---- down flush: M_ij = sum over the block rows r = s0-j .. s1-j of L_ir E_rj
+        Ep[w:w + m, :] = torch.where((ii + jj >= s0) & (ii + jj <= s1), E, torch.zeros((), dtype=dt, device=dev))
+        M = torch.empty_like(X)
+        for c0 in range(0, n, chunk):
+            js = torch.arange(c0, min(n, c0 + chunk), device=dev)
+            r0 = s0 - js  # first block row of column j (may be negative)
+            # rows outside the matrix land in the zero padding (clamped there)
+            cols = (r0[:, None] + ar_w[None, :] + w).clamp(0, m + 2 * w - 1)
+            Lw = Lp[:, cols]                              # m x nj x w: the shifting windows of L
+            Ew = Ep[cols, js[:, None]]                    # nj x w
+            M[:, js] = torch.bmm(Lw.permute(1, 0, 2).contiguous(), Ew[:, :, None].contiguous())[:, :, 0].T
+        M = torch.where(later, M, torch.zeros((), dtype=dt, device=dev))
+        C += M
+        Y += M
+        # ---- right flush: Y_ij += sum over the block columns t = s0-i .. s1-i of C_it U_tj
+        Cp[:, w:w + n] = torch.where((ii + jj >= s0) & (ii + jj <= s1), C, torch.zeros((), dtype=dt, device=dev))
+        for r0_ in range(0, m, chunk):
+            is_ = torch.arange(r0_, min(m, r0_ + chunk), device=dev)
+            t0 = s0 - is_
+            rows = (t0[:, None] + ar_w[None, :] + w).clamp(0, n + 2 * w - 1)
+            Uw = Up[rows, :]                              # ni x w x n: the shifting windows of U
+            Cw = Cp[is_[:, None], rows]                   # ni x w
+            V = torch.bmm(Cw[:, None, :].contiguous(), Uw.contiguous())[:, 0, :]
+            Y[is_, :] += torch.where(later[is_, :], V, torch.zeros((), dtype=dt, device=dev))
+    return Z, Y, E

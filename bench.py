@@ -128,6 +128,59 @@ def cpu_baseline(prob, sample: int, reverse: bool = False):
     }
 
 
+def array_baseline_run(prob, sample: int, w: int, dev):
+    """The paper's own array-framework realisation of the sweep (Algorithm 4 in
+    PyTorch, array_baseline.py) timed on the GPU on the leading sample x sample
+    block, next to the HIP sweep on the same block; both use the library's
+    factors of that block. Scaled to the workload by mn(m+n)."""
+    import numpy as np
+    import torch
+
+    import array_baseline as ab
+    from paper_2607_27042_amd import binding
+
+    s_m, s_n = min(sample, prob.m), min(sample, prob.n)
+    X = torch.from_numpy(np.ascontiguousarray(prob.X[:s_m, :s_n])).to(dev)
+    A = torch.from_numpy(np.ascontiguousarray(prob.A[:s_m, :s_m])).to(dev)
+    B = torch.from_numpy(np.ascontiguousarray(prob.B[:s_n, :s_n])).to(dev)
+    f = binding.Factors.from_bases(A, B)
+    L, U, _, _ = f.export()
+    ws = f.workspace()
+    Zh = torch.empty((s_m, s_n), dtype=torch.int32, device=dev)
+    Yh = torch.empty_like(X)
+    obj = torch.empty(1, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+    binding.gptq2d_round(f.handle, X, Zh, Yh, obj, ws, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(5):
+        binding.gptq2d_round(f.handle, X, Zh, Yh, obj, ws, stream)
+    torch.cuda.synchronize()
+    t_hip = (time.perf_counter() - t0) / 5
+    X64 = X.double()
+    ab.blocked_sweep(X64[:64, :64].contiguous(), L[:64, :64].contiguous(), U[:64, :64].contiguous(), w=w)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    Za, _, _ = ab.blocked_sweep(X64, L, U, w=w)
+    torch.cuda.synchronize()
+    t_arr = time.perf_counter() - t0
+    mism = int((Za.to(torch.int32) != Zh).sum())
+    f.close()
+    m, n = prob.m, prob.n
+    scale = (m * n * (m + n)) / (s_m * s_n * (s_m + s_n))
+    return {
+        "value": m * n / (t_arr * scale),
+        "unit": "entries/s",
+        "kind": "paper Algorithm 4 (blocked, band flushes as windowed batched mat-vecs) in PyTorch fp64 on the GPU",
+        "sample": f"leading {s_m}x{s_n} block, block width {w}, the library's factors of that block; "
+                  f"scaled by mn(m+n) to {m}x{n}",
+        "sweep_s": t_arr,
+        "hip_sweep_s_same_sample": t_hip,
+        "hip_speedup": t_arr / t_hip,
+        "z_mismatches_vs_hip": mism,
+    }
+
+
 def _cpu_model():
     try:
         with open("/proc/cpuinfo") as fh:
@@ -227,6 +280,11 @@ def main():
     ap.add_argument("--dtype", default=None)
     ap.add_argument("--cpu-sample", type=int, default=1536)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--array-baseline", type=int, default=0, metavar="S",
+                    help="also time the paper's own array-framework realisation (Algorithm 4 in "
+                         "PyTorch) on the GPU on the leading S x S block")
+    ap.add_argument("--array-block", type=int, default=64, metavar="W",
+                    help="block width of that realisation")
     ap.add_argument("--batch", type=int, default=1, metavar="N",
                     help="N problems of the config (the layers of one model, each with its own X "
                          "and bases) per step, factorised and rounded by the batched entry points")
@@ -365,6 +423,9 @@ def main():
                             "flop": factor_flop},
         "objective": float(obj.cpu()[0]),
     }
+    if args.array_baseline > 0:
+        log(f"array-framework realisation on the leading {args.array_baseline} block")
+        out["array_baseline"] = array_baseline_run(prob, args.array_baseline, args.array_block, dev)
     if not args.no_cpu_baseline:
         log(f"cpu baseline on a {args.cpu_sample} sample")
         out["cpu_baseline"] = cpu_baseline(prob, args.cpu_sample, args.order == "reverse")
