@@ -412,3 +412,55 @@ def test_replay_follows_hint_trajectory():
     assert c["hard"] >= 1 and hard[0] == 0
     E = Zr - Yr
     assert np.abs((Zr - X) - L @ E @ U).max() < 1e-10
+
+
+def _read_fig1():
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "fig1_dependency_3x4.txt")
+    out = {}
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        key, *rest = line.split()
+        out[key] = rest
+    return out
+
+
+def test_fig1_dependency_graph():
+    """Fig. 1's 3 x 4 example (tests/golden/fig1_dependency_3x4.txt): an entry's
+    rounding depends on X only through the entries that reach it along the
+    arrows (i' <= i, j' <= j). A large change of X at one entry leaves every
+    unreachable entry's Z unchanged, in particular the other entries of the red
+    anti-diagonal I_4, and the sweep visits m + n - 1 anti-diagonals."""
+    g = _read_fig1()
+    m, n = int(g["shape"][0]), int(g["shape"][1])
+    assert int(g["wavefronts"][0]) == m + n - 1
+    s_red = int(g["red_set"][0])
+    red = [tuple(int(v) for v in e.split(",")) for e in g["red_set"][1:]]
+    assert sorted(red) == sorted((i, s_red - i) for i in range(1, m + 1) if 1 <= s_red - i <= n)
+    rng = np.random.default_rng(7)
+    A = np.triu(rng.standard_normal((m, m))) + 3 * np.eye(m)
+    A = A + 0.5 * rng.standard_normal((m, m))
+    B = np.tril(rng.standard_normal((n, n))) + 3 * np.eye(n)
+    B = B + 0.5 * rng.standard_normal((n, n))
+    L, lamL, U, lamU = oracle.factors(A, B)
+    X = 3 * rng.standard_normal((m, n))
+    Z0 = oracle.round_nested(X, L, U)[0]
+    changed_somewhere = False
+    for (i1, j1) in [(a, b) for a in range(1, m + 1) for b in range(1, n + 1)]:
+        Xp = X.copy()
+        Xp[i1 - 1, j1 - 1] += 7.3
+        Zp = oracle.round_nested(Xp, L, U)[0]
+        for i in range(1, m + 1):
+            for j in range(1, n + 1):
+                reachable = i >= i1 and j >= j1
+                if not reachable:
+                    assert Zp[i - 1, j - 1] == Z0[i - 1, j - 1], ((i1, j1), (i, j))
+                elif (i, j) != (i1, j1) and Zp[i - 1, j - 1] != Z0[i - 1, j - 1]:
+                    changed_somewhere = True
+        if (i1, j1) in red:  # the red set is mutually unreachable
+            for (i, j) in red:
+                if (i, j) != (i1, j1):
+                    assert Zp[i - 1, j - 1] == Z0[i - 1, j - 1]
+    # the feedback does reach later entries (a sweep without pushes would not)
+    assert changed_somewhere
