@@ -217,13 +217,18 @@ def run_batch(args, dev):
     fws = torch.empty(binding.gptq2d_factor_batched_workspace_size(N), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
+    # the argument arrays are built once (a loop over the same tensors)
+    factor_call = binding.gptq2d_factor_batched(handles, As, Bs, fws, stream, shapes=shapes, prepare=True)
+    round_call = binding.gptq2d_round_batched(handles, Xs, Zs, Ys, obj, ws, stream, shapes=shapes,
+                                              prepare=True)
+
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        binding.gptq2d_factor_batched(handles, As, Bs, fws, stream, shapes=shapes)
+        factor_call()
         if ev is not None:
             ev[1].record(stream)
-        binding.gptq2d_round_batched(handles, Xs, Zs, Ys, obj, ws, stream, shapes=shapes)
+        round_call()
         if ev is not None:
             ev[2].record(stream)
 
@@ -247,7 +252,7 @@ def run_batch(args, dev):
     t_fac = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
     t_round = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
     out = {
-        "metric": METRIC,
+        "metric": "rounded entries/s (a batch of problems per step)",
         "value": N * m * n / (ms_step * 1e-3),
         "unit": "entries/s",
         "n_gpus": 1,
@@ -390,7 +395,7 @@ def main():
     value = m * n / (ms_step * 1e-3)
 
     out = {
-        "metric": METRIC,
+        "metric": METRIC if args.config == 3 else f"rounded entries/s at the c{args.config} workload",
         "value": value,
         "unit": "entries/s",
         "n_gpus": 1,

@@ -175,9 +175,10 @@ def gptq2d_factor_batched_workspace_size(count: int) -> int:
     return int(load().gptq2d_factor_batched_workspace_size(count))
 
 
-def gptq2d_factor_batched(handles, As, Bs, workspace: torch.Tensor, stream=None, shapes=None) -> None:
+def gptq2d_factor_batched(handles, As, Bs, workspace: torch.Tensor, stream=None, shapes=None,
+                          prepare=False):
     """Factorisations of len(handles) problems (distinct handles) in common
-    launches per shape."""
+    launches per shape. prepare=True: as for gptq2d_round_batched."""
     count = len(handles)
     if count == 0 or len(As) != count or len(Bs) != count:
         raise ValueError("one A and one B per handle")
@@ -191,9 +192,15 @@ def gptq2d_factor_batched(handles, As, Bs, workspace: torch.Tensor, stream=None,
         b, lb = _mat(Bs[p], n, n, f"B[{p}]")
         ap.append(a.value); al.append(la); bp.append(b.value); bl.append(lb)
     VP, I64 = ctypes.c_void_p * count, ctypes.c_int64 * count
-    _check(load().gptq2d_factor_batched(count, _handles(handles), dt, VP(*ap), I64(*al), VP(*bp), I64(*bl),
-                                        _ptr(workspace), workspace.numel() * workspace.element_size(),
-                                        _stream(stream)), "gptq2d_factor_batched")
+    args = (count, _handles(handles), dt, VP(*ap), I64(*al), VP(*bp), I64(*bl), _ptr(workspace),
+            workspace.numel() * workspace.element_size(), _stream(stream))
+    fn = load().gptq2d_factor_batched
+
+    def call():
+        _check(fn(*args), "gptq2d_factor_batched")
+    if prepare:
+        return call
+    call()
 
 
 def gptq2d_factor_batched_check(handles, stream=None) -> None:
@@ -277,10 +284,12 @@ def gptq2d_round_batched_workspace_size(handles) -> int:
 
 
 def gptq2d_round_batched(handles, Xs, Zs, Ys, objective, workspace: torch.Tensor, stream=None,
-                         shapes=None) -> None:
+                         shapes=None, prepare=False):
     """Problems p = 0 .. len(handles)-1 in common launches; Ys may be None (or
     hold None entries); objective None or a float64 device tensor of
-    len(handles) entries."""
+    len(handles) entries. With prepare=True nothing is enqueued: the argument
+    arrays are built once and a function of no arguments is returned that
+    enqueues the call (for loops over the same tensors)."""
     count = len(handles)
     if not (len(Xs) == len(Zs) == count) or (Ys is not None and len(Ys) != count):
         raise ValueError("one X, Z (and Y) per handle")
@@ -312,10 +321,15 @@ def gptq2d_round_batched(handles, Xs, Zs, Ys, objective, workspace: torch.Tensor
     X_a, ldx_a, Z_a, ldz_a = VP(*xp), I64(*xl), VP(*zp), I64(*zl)
     Y_a = VP(*yp) if Ys is not None else None
     ldy_a = I64(*yl) if Ys is not None else None
-    _check(load().gptq2d_round_batched(count, _handles(handles), dt, X_a, ldx_a, Z_a, ldz_a, Y_a, ldy_a,
-                                       _ptr(objective), _ptr(workspace),
-                                       workspace.numel() * workspace.element_size(), _stream(stream)),
-           "gptq2d_round_batched")
+    args = (count, _handles(handles), dt, X_a, ldx_a, Z_a, ldz_a, Y_a, ldy_a, _ptr(objective),
+            _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+    fn = load().gptq2d_round_batched
+
+    def call():
+        _check(fn(*args), "gptq2d_round_batched")
+    if prepare:
+        return call
+    call()
 
 
 def gptq2d_round_batched_check(workspace: torch.Tensor, stream=None) -> None:
