@@ -208,3 +208,33 @@ def test_factor_batched_errors():
     binding.gptq2d_factor_batched_check([fa.handle])
     fa.close()
     fb.close()
+
+
+def test_prepared_batched_calls_repeat():
+    """The prepared form (argument arrays built once) enqueues the same calls:
+    two invocations after changing X in place give the results of direct calls."""
+    probs = [wl.random_problem(96, 70, 50 + i, "f64", "wishart") for i in range(3)]
+    fs = [binding.Factors(p.m, p.n) for p in probs]
+    As = [pr.to_dev(p.A) for p in probs]
+    Bs = [pr.to_dev(p.B) for p in probs]
+    Xs = [pr.to_dev(p.X) for p in probs]
+    handles = [f.handle for f in fs]
+    fws = torch.empty(binding.gptq2d_factor_batched_workspace_size(3), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(binding.gptq2d_round_batched_workspace_size(handles), dtype=torch.uint8, device="cuda")
+    Zs = [torch.empty((p.m, p.n), dtype=torch.int32, device="cuda") for p in probs]
+    obj = torch.empty(3, dtype=torch.float64, device="cuda")
+    fcall = binding.gptq2d_factor_batched(handles, As, Bs, fws, prepare=True)
+    rcall = binding.gptq2d_round_batched(handles, Xs, Zs, None, obj, ws, prepare=True)
+    for rep in range(2):
+        if rep == 1:
+            for X in Xs:
+                X.mul_(1.5)
+        fcall()
+        rcall()
+        binding.gptq2d_round_batched_check(ws)
+        for i, f in enumerate(fs):
+            Z1, _, o1 = _single(f, Xs[i])
+            assert np.array_equal(Zs[i].cpu().numpy(), Z1), (rep, i)
+            assert float(obj[i]) == o1, (rep, i)
+    for f in fs:
+        f.close()
