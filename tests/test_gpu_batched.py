@@ -238,3 +238,40 @@ def test_prepared_batched_calls_repeat():
             assert float(obj[i]) == o1, (rep, i)
     for f in fs:
         f.close()
+
+
+@pytest.mark.parametrize("reverse", [False, True])
+def test_padded_leading_dimensions(reverse):
+    """X, Z, Y as views into wider buffers (leading dimension > n), in both
+    orders, single and batched: the same results as contiguous tensors."""
+    p = wl.random_problem(150, 70, 77, "f32", "wishart")
+    f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B), reverse=reverse)
+    X = pr.to_dev(p.X)
+    Z0, Y0, o0 = binding.round_matrix(f, X)
+    wide = torch.full((150, 97), float("nan"), dtype=torch.float32, device="cuda")
+    wide[:, 5:75] = X
+    Xv = wide[:, 5:75]
+    Zb = torch.full((150, 90), -7, dtype=torch.int32, device="cuda")
+    Yb = torch.full((150, 81), float("nan"), dtype=torch.float32, device="cuda")
+    Zv, Yv = Zb[:, 3:73], Yb[:, 2:72]
+    obj = torch.empty(1, dtype=torch.float64, device="cuda")
+    binding.gptq2d_round(f.handle, Xv, Zv, Yv, obj, f.workspace())
+    binding.gptq2d_round_check(f.handle, f.workspace())
+    torch.cuda.synchronize()
+    assert torch.equal(Zv, Z0) and torch.equal(Yv, Y0) and float(obj[0]) == float(o0[0])
+    # nothing outside the views was written
+    assert bool((Zb[:, :3] == -7).all()) and bool((Zb[:, 73:] == -7).all())
+    assert bool(torch.isnan(Yb[:, :2]).all()) and bool(torch.isnan(Yb[:, 72:]).all())
+    # batched, the same views twice over two workspaces' worth of problems
+    Zv2 = torch.empty_like(Z0)
+    Zs, Ys, objs = [Zv, Zv2], [Yv, None], torch.empty(2, dtype=torch.float64, device="cuda")
+    Zv.fill_(0)
+    ws = torch.empty(binding.gptq2d_round_batched_workspace_size([f.handle, f.handle]), dtype=torch.uint8,
+                     device="cuda")
+    binding.gptq2d_round_batched([f.handle, f.handle], [Xv, X], Zs, Ys, objs, ws)
+    binding.gptq2d_round_batched_check(ws)
+    torch.cuda.synchronize()
+    assert torch.equal(Zv, Z0) and torch.equal(Zv2, Z0) and torch.equal(Yv, Y0)
+    assert float(objs[0]) == float(o0[0]) == float(objs[1])
+    assert bool((Zb[:, :3] == -7).all()) and bool((Zb[:, 73:] == -7).all())
+    f.close()
