@@ -117,6 +117,10 @@ gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
     st = alloc(f, &p, 256);
     if (st == GPTQ2D_OK) {
       f->flags = (int*)p;
+      st = alloc(f, &f->d_fac, fac_static_bytes());
+    }
+    if (st == GPTQ2D_OK) st = upload_fac_static(*f);
+    if (st == GPTQ2D_OK) {
       he = hipMemset(f->flags, 0, 256);
       if (he != hipSuccess) st = hip_fail(he, "hipMemset");
     }

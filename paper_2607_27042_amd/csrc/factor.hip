@@ -46,15 +46,18 @@ struct FacArgs {
 
 // Batched factorisation: problems of one shape in common launches. Problem p
 // owns the blocks p per .. p per + per - 1 of a launch (per = the grid of a
-// single problem's launch) and takes its FacArgs and inputs from a device
-// table; every block then does exactly what it does in a single problem's
-// launch, so the results are the same bits.
+// single problem's launch) and takes its inputs from a device table, its
+// FacArgs from its handle's copy on the device; every block then does exactly
+// what it does in a single problem's launch, so the results are the same bits.
+struct FacStatic {  // fixed per handle
+  FacArgs f;        // (f.rev unused: the order is the problem's)
+  double* gpart;
+};
 struct FacProb {
-  FacArgs f;
+  const FacStatic* base;
   const void* A;
   const void* B;
-  int64_t lda, ldb;
-  double* gpart;
+  int64_t lda, ldb, rev;
 };
 struct BatchCtx {
   const FacProb* tab;  // unused by single-problem launches
@@ -186,19 +189,20 @@ __global__ __launch_bounds__(NT) void k_gram(FacArgs f0, const T* A0, int64_t ld
                                              int64_t ldb0, int sides, BatchCtx bc) {
   __shared__ Stage64 st;
   const FacProb* pb = bat_prob<BAT>(bc);
-  const FacArgs& f = BAT ? pb->f : f0;
+  const FacArgs& f = BAT ? pb->base->f : f0;
   const T* A = BAT ? (const T*)pb->A : A0;
   const T* B = BAT ? (const T*)pb->B : B0;
   const int64_t lda = BAT ? pb->lda : lda0, ldb = BAT ? pb->ldb : ldb0;
   const int bid = bat_block<BAT>(bc);
+  const int rev = BAT ? (int)pb->rev : f0.rev;
   const int t0 = (sides & 1) ? f.s[0].nb * (f.s[0].nb + 1) / 2 : 0;
   int bp, bq;
   if (bid < t0) {
     tri_index(bid, bp, bq);
-    gram_tile<T, 0>(f.s[0], A, lda, bp, bq, st, f.rev);
+    gram_tile<T, 0>(f.s[0], A, lda, bp, bq, st, rev);
   } else {
     tri_index(bid - t0, bp, bq);
-    gram_tile<T, 1>(f.s[1], B, ldb, bp, bq, st, f.rev);
+    gram_tile<T, 1>(f.s[1], B, ldb, bp, bq, st, rev);
   }
 }
 
@@ -233,7 +237,7 @@ __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f0, const T* A0, int64
                                                   int64_t ldb0, int sides, BatchCtx bc) {
   __shared__ double tile[TB][TB + 1];
   const FacProb* pb = bat_prob<BAT>(bc);
-  const FacArgs& f = BAT ? pb->f : f0;
+  const FacArgs& f = BAT ? pb->base->f : f0;
   const T* A = BAT ? (const T*)pb->A : A0;
   const T* B = BAT ? (const T*)pb->B : B0;
   const int64_t lda = BAT ? pb->lda : lda0, ldb = BAT ? pb->ldb : ldb0;
@@ -246,7 +250,7 @@ __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f0, const T* A0, int64
   const int i0 = (b / nt) * TB, k0 = (b % nt) * TB;  // S rows i0.., columns k0..
   double* S = sd.li;
   const int t = threadIdx.x;
-  const int rev = f.rev;
+  const int rev = BAT ? (int)pb->rev : f0.rev;
   if (side == 0) {
     // A rows k0 + r, columns d-1-(i0+63) .. d-1-i0 (ascending; in reverse
     // order i0 .. i0+63), coalesced
@@ -402,8 +406,8 @@ template <bool BAT>
 __global__ __launch_bounds__(NT) void k_gram128(FacArgs f0, GramPlan pl, double* part0, BatchCtx bc) {
   __shared__ GramChunk buf[2];
   const FacProb* pb = bat_prob<BAT>(bc);
-  const FacArgs& f = BAT ? pb->f : f0;
-  double* part = BAT ? pb->gpart : part0;
+  const FacArgs& f = BAT ? pb->base->f : f0;
+  double* part = BAT ? pb->base->gpart : part0;
   const int bid = bat_block<BAT>(bc);
   // work groups are dealt round-robin to the eight L2 domains (XCDs): give
   // each domain a contiguous run of ranges, so that the tiles it runs at the
@@ -445,8 +449,8 @@ __global__ __launch_bounds__(NT) void k_gram128(FacArgs f0, GramPlan pl, double*
 template <bool BAT>
 __global__ __launch_bounds__(NT) void k_gram_fix(FacArgs f0, GramPlan pl, const double* part0, BatchCtx bc) {
   const FacProb* pb = bat_prob<BAT>(bc);
-  const FacArgs& f = BAT ? pb->f : f0;
-  const double* part = BAT ? pb->gpart : part0;
+  const FacArgs& f = BAT ? pb->base->f : f0;
+  const double* part = BAT ? pb->base->gpart : part0;
   const int jr = bat_block<BAT>(bc);
   const int64_t u = pl.lo(jr + 1);
   int side, b, c;
@@ -709,7 +713,7 @@ __device__ void diag_tile(const Side& sd, int kb, int* flags, DiagSmem& ds) {
 template <bool BAT>
 __global__ __launch_bounds__(NT) void k_diag(FacArgs f0, int kb, BatchCtx bc) {
   __shared__ DiagSmem ds;
-  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->base->f : f0;
   const Side& sd = f.s[bat_block<BAT>(bc)];
   if (kb >= sd.nb) return;
   diag_tile(sd, kb, f.flags, ds);
@@ -729,7 +733,7 @@ __device__ __forceinline__ int panel_count(const Side& sd, int kb) {
 template <bool BAT>
 __global__ __launch_bounds__(NT) void k_panel(FacArgs f0, int kb, BatchCtx bc) {
   __shared__ Stage64 st;
-  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->base->f : f0;
   int b = bat_block<BAT>(bc);
   const int n0 = panel_count(f.s[0], kb);
   const Side& sd = (b < n0) ? f.s[0] : f.s[1];
@@ -810,7 +814,7 @@ __global__ __launch_bounds__(NT) void k_update(FacArgs f0, UpdRange r, BatchCtx 
     DiagSmem d;
   } sm;
   Stage64* st = sm.st;
-  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->base->f : f0;
   int b = bat_block<BAT>(bc);
   int nq0, ns0;
   upd_counts(f.s[0], r, nq0, ns0);
@@ -1042,7 +1046,7 @@ __device__ void update128_tile(const FacArgs& f, int g0, int g1, int g2, int b, 
 template <bool BAT>
 __global__ __launch_bounds__(NT) void k_update128(FacArgs f0, int g0, int g1, int g2, int ntile, BatchCtx bc) {
   __shared__ UpdChunk buf[2];
-  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->base->f : f0;
   const int bid = bat_block<BAT>(bc), grid = bat_grid<BAT>(bc);
   for (int b = bid; b < ntile; b += grid) {
     if (b != bid) __syncthreads();  // the staging buffers are reused
@@ -1063,7 +1067,7 @@ template <bool BAT>
 __global__ __launch_bounds__(NT) void k_finalize(FacArgs f0, BatchCtx bc) {
   __shared__ double S[TB][TB + 1];
   __shared__ double sc[TB];
-  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->f : f0;
+  const FacArgs& f = BAT ? bat_prob<BAT>(bc)->base->f : f0;
   const int bid = bat_block<BAT>(bc);
   const int t0 = f.s[0].nb * (f.s[0].nb + 1) / 2;
   const int side = bid < t0 ? 0 : 1;
@@ -1104,7 +1108,7 @@ __global__ __launch_bounds__(NT) void k_finalize(FacArgs f0, BatchCtx bc) {
 
 __global__ void k_zero_flags_batch(const FacProb* tab, int count) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
-  if (p < count) tab[p].f.flags[0] = 0;
+  if (p < count) tab[p].base->f.flags[0] = 0;
 }
 
 // Stream-ordered upload of up to PUT_WORDS 8-byte words that travel as
@@ -1375,19 +1379,24 @@ gptq2d_status launch_factor(Factors& f, gptq2d_dtype dt, const void* A, int64_t 
 
 size_t factor_batch_table_bytes(int count) { return (size_t)count * sizeof(FacProb); }
 
+size_t fac_static_bytes() { return sizeof(FacStatic); }
+
+gptq2d_status upload_fac_static(Factors& f) {
+  FacStatic s;
+  s.f = fac_args(f);
+  s.f.rev = 0;
+  s.gpart = f.gpart;
+  hipError_t e = hipMemcpy(f.d_fac, &s, sizeof(s), hipMemcpyHostToDevice);
+  return e == hipSuccess ? GPTQ2D_OK : hip_fail(e, "handle upload");
+}
+
 gptq2d_status launch_factor_batched(int count, Factors* const* fs, gptq2d_dtype dt,
                                     const void* const* A, const int64_t* lda, const void* const* B,
                                     const int64_t* ldb, void* table, hipStream_t s) {
   static_assert(sizeof(FacProb) % sizeof(uint64_t) == 0, "the table is uploaded in 8-byte words");
   std::vector<FacProb> h(count);
-  for (int p = 0; p < count; ++p) {
-    h[p].f = fac_args(*fs[p]);
-    h[p].A = A[p];
-    h[p].B = B[p];
-    h[p].lda = lda[p];
-    h[p].ldb = ldb[p];
-    h[p].gpart = fs[p]->gpart;
-  }
+  for (int p = 0; p < count; ++p)
+    h[p] = FacProb{(const FacStatic*)fs[p]->d_fac, A[p], B[p], lda[p], ldb[p], fs[p]->rev};
   gptq2d_status st = enqueue_upload(table, h.data(), h.size() * sizeof(FacProb), s);
   if (st != GPTQ2D_OK) return st;
   return factor_impl(*fs[0], (const FacProb*)table, count, dt, nullptr, 0, nullptr, 0, s);

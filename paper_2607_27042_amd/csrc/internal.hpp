@@ -24,6 +24,7 @@ struct Schedule {
   int4* d_tasks = nullptr;       // all tasks, grouped by stage, then by bin
   int4* d_bins = nullptr;        // {first task in the stage, counts by shape}, grouped by stage
   int4* d_stage = nullptr;       // per stage: {offset, bin_offset, bins, 0} (batched rounding)
+  void* d_base = nullptr;        // the handle's fixed stage arguments on the device (batched rounding)
   size_t ntasks = 0;
 };
 
@@ -62,6 +63,9 @@ struct Factors {
   bool stage_timing = false;
   mutable std::vector<hipEvent_t> stage_ev;  // event pool, grows on demand
   mutable size_t stage_ev_used = 0;          // events recorded since the last read
+  // the handle's fixed factorisation arguments on the device (batched
+  // factorisation), fac_static_bytes() bytes
+  void* d_fac = nullptr;
   std::vector<void*> allocations;
 };
 
@@ -74,6 +78,22 @@ struct Workspace {
   double* E;     // rounding errors, mp x np
   double* C;     // the buffer C = L E, mp x np
 };
+// the layout itself, on the host and on the device (a batched sweep finds
+// each problem's buffers in its workspace region)
+__host__ __device__ inline Workspace carve_workspace(void* base, int mp, int np, int MT, int NT) {
+  char* p = (char*)base;
+  Workspace w;
+  w.flags = (int*)p;
+  p += 256;
+  w.objp = (double*)p;
+  p += ((size_t)MT * NT * sizeof(double) + 255) / 256 * 256;
+  const size_t tile = (size_t)mp * np * sizeof(double);
+  w.P = (double*)p;
+  w.R = (double*)(p + tile);
+  w.E = (double*)(p + 2 * tile);
+  w.C = (double*)(p + 3 * tile);
+  return w;
+}
 size_t workspace_bytes(const Factors& f);
 Workspace workspace_carve(const Factors& f, void* base);
 
@@ -91,6 +111,9 @@ gptq2d_status enqueue_upload(void* dst, const void* src, size_t bytes, hipStream
 // events order it); `table` holds factor_batch_table_bytes(count) bytes of
 // device memory
 size_t factor_batch_table_bytes(int count);
+// the handle's fixed factorisation arguments, copied to f.d_fac (synchronous)
+size_t fac_static_bytes();
+gptq2d_status upload_fac_static(Factors& f);
 gptq2d_status launch_factor_batched(int count, Factors* const* fs, gptq2d_dtype dt,
                                     const void* const* A, const int64_t* lda, const void* const* B,
                                     const int64_t* ldb, void* table, hipStream_t s);

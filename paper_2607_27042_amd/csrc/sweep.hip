@@ -728,14 +728,43 @@ __global__ __launch_bounds__(NT) void k_stage(StageArgs a) {
 // work groups of every problem that has a stage k: problem p owns the blocks
 // off[p] .. off[p+1]-1 and runs them exactly as k_stage would, so the merged
 // launch has the work of all problems in flight at once (small problems
-// occupy a few compute units each). Problem p's StageArgs (stage fields
-// unset) live in a device table.
+// occupy a few compute units each). Problem p's record in a device table
+// holds what differs between calls; the rest of its StageArgs is its
+// handle's, kept on the device with the handle.
 constexpr int BATCH_MAX = 512;  // problems per launch (block offsets travel as kernel arguments)
+struct BatchProb {
+  const StageArgs* base;  // the handle's fixed part (shape, factors, plan)
+  const void* X;
+  int32_t* Z;
+  void* Y;
+  int64_t ldx, ldz, ldy, cstep;
+  void* ws;  // the problem's workspace region (layout of carve_workspace)
+};
 struct BatchLaunch {
-  const StageArgs* desc;
+  const BatchProb* desc;
+  int* flags;  // the batch's error word
   int count, stage;
   int off[BATCH_MAX + 1];
 };
+
+__device__ __forceinline__ StageArgs batch_args(const BatchProb& q, int* flags) {
+  StageArgs a = *q.base;
+  a.X = q.X;
+  a.ldx = q.ldx;
+  a.Z = q.Z;
+  a.ldz = q.ldz;
+  a.Y = q.Y;
+  a.ldy = q.ldy;
+  a.cstep = (int)q.cstep;
+  const Workspace w = carve_workspace(q.ws, a.mp, a.np, a.MT, a.NT);
+  a.objp = w.objp;
+  a.P = w.P;
+  a.R = w.R;
+  a.E = w.E;
+  a.C = w.C;
+  a.flags = flags;
+  return a;
+}
 
 template <typename T>
 __global__ __launch_bounds__(NT) void k_stage_batch(BatchLaunch bl) {
@@ -748,7 +777,7 @@ __global__ __launch_bounds__(NT) void k_stage_batch(BatchLaunch bl) {
     if (bl.off[mid] <= b) lo = mid;
     else hi = mid - 1;
   }
-  StageArgs a = bl.desc[lo];
+  StageArgs a = batch_args(bl.desc[lo], bl.flags);
   const int k = bl.stage, lb = b - bl.off[lo];
   const int4 st = a.stab[k];
   a.stage = k;
@@ -766,12 +795,13 @@ __global__ __launch_bounds__(NT) void k_stage_batch(BatchLaunch bl) {
 
 // Objective of every problem of a batch: block p sums problem p's per-tile
 // partials in a fixed order.
-__global__ __launch_bounds__(NT) void k_obj_reduce_batch(const StageArgs* desc, double* out) {
+__global__ __launch_bounds__(NT) void k_obj_reduce_batch(const BatchProb* desc, double* out) {
   __shared__ double red[NT];
-  const StageArgs& a = desc[blockIdx.x];
-  const int count = a.MT * a.NT;
+  const BatchProb& q = desc[blockIdx.x];
+  const int count = q.base->MT * q.base->NT;
+  const double* objp = carve_workspace(q.ws, q.base->mp, q.base->np, q.base->MT, q.base->NT).objp;
   double s = 0.0;
-  for (int i = threadIdx.x; i < count; i += NT) s += a.objp[i];
+  for (int i = threadIdx.x; i < count; i += NT) s += objp[i];
   red[threadIdx.x] = s;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -810,18 +840,7 @@ size_t workspace_bytes(const Factors& f) {
 }
 
 Workspace workspace_carve(const Factors& f, void* base) {
-  char* p = (char*)base;
-  Workspace w;
-  w.flags = (int*)p;
-  p += 256;
-  w.objp = (double*)p;
-  p += align256((size_t)f.MT * f.NT * sizeof(double));
-  const size_t tile = (size_t)f.mp * f.np * sizeof(double);
-  w.P = (double*)p;
-  w.R = (double*)(p + tile);
-  w.E = (double*)(p + 2 * tile);
-  w.C = (double*)(p + 3 * tile);
-  return w;
+  return carve_workspace(base, f.mp, f.np, f.MT, f.NT);
 }
 
 // Delivery plan of the deferred feedback. Targets are grouped in 2 x 2
@@ -1036,9 +1055,11 @@ void free_schedule(Schedule& sc) {
   if (sc.d_tasks) (void)hipFree(sc.d_tasks);
   if (sc.d_bins) (void)hipFree(sc.d_bins);
   if (sc.d_stage) (void)hipFree(sc.d_stage);
+  if (sc.d_base) (void)hipFree(sc.d_base);
   sc.d_tasks = nullptr;
   sc.d_bins = nullptr;
   sc.d_stage = nullptr;
+  sc.d_base = nullptr;
 }
 
 gptq2d_status build_schedule(Factors& f, int g) {
@@ -1072,6 +1093,25 @@ gptq2d_status build_schedule(Factors& f, int g) {
     hipError_t e = hipMalloc(&f.sched.d_stage, S * sizeof(int4));
     if (e != hipSuccess) return hip_fail(e, "schedule allocation");
     e = hipMemcpy(f.sched.d_stage, stab.data(), S * sizeof(int4), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "schedule upload");
+    // the fixed stage arguments of the handle (batched rounding)
+    StageArgs b{};
+    b.m = f.m;
+    b.n = f.n;
+    b.mp = f.mp;
+    b.np = f.np;
+    b.MT = f.MT;
+    b.NT = f.NT;
+    b.L = f.L;
+    b.U = f.U;
+    b.dL = f.dL;
+    b.dU = f.dU;
+    b.tasks = f.sched.d_tasks;
+    b.bins = f.sched.d_bins;
+    b.stab = f.sched.d_stage;
+    e = hipMalloc(&f.sched.d_base, sizeof(StageArgs));
+    if (e != hipSuccess) return hip_fail(e, "schedule allocation");
+    e = hipMemcpy(f.sched.d_base, &b, sizeof(StageArgs), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_fail(e, "schedule upload");
   }
   f.sched.g = g;
@@ -1178,7 +1218,7 @@ gptq2d_status launch_round(const Factors& f, gptq2d_dtype dt, const void* X, int
 
 // Workspace of a batch: the batch's error flags (256 bytes), the problems'
 // StageArgs table, then one gptq2d_round workspace region per problem.
-static size_t batch_table_bytes(int count) { return align256((size_t)count * sizeof(StageArgs)); }
+static size_t batch_table_bytes(int count) { return align256((size_t)count * sizeof(BatchProb)); }
 
 size_t batched_workspace_bytes(int count, const Factors* const* f) {
   size_t b = 256 + batch_table_bytes(count);
@@ -1191,23 +1231,21 @@ static gptq2d_status round_batched_typed(int count, const Factors* const* f, con
                                          const int64_t* ldx, int32_t* const* Z, const int64_t* ldz,
                                          void* const* Y, const int64_t* ldy, double* objective,
                                          void* workspace, hipStream_t s) {
-  static_assert(sizeof(StageArgs) % sizeof(uint64_t) == 0, "the table is uploaded in 8-byte words");
+  static_assert(sizeof(BatchProb) % sizeof(uint64_t) == 0, "the table is uploaded in 8-byte words");
   char* base = (char*)workspace;
   int* flags = (int*)base;
-  StageArgs* desc = (StageArgs*)(base + 256);
+  BatchProb* desc = (BatchProb*)(base + 256);
   char* region = base + 256 + batch_table_bytes(count);
-  std::vector<StageArgs> h(count);
+  std::vector<BatchProb> h(count);
   for (int p = 0; p < count; ++p) {
     const Workspace ws = workspace_carve(*f[p], region);
+    // X, Z, Y as the problem's sweep addresses them (mirrored in reverse order)
+    const StageArgs a = stage_args<T>(*f[p], X[p], ldx[p], Z[p], ldz[p], Y ? Y[p] : nullptr, Y ? ldy[p] : 0, ws);
+    h[p] = BatchProb{(const StageArgs*)f[p]->sched.d_base, a.X, a.Z, a.Y, a.ldx, a.ldz, a.ldy, a.cstep, region};
     region += align256(workspace_bytes(*f[p]));
-    h[p] = stage_args<T>(*f[p], X[p], ldx[p], Z[p], ldz[p], Y ? Y[p] : nullptr, Y ? ldy[p] : 0, ws);
-    h[p].flags = flags;
-    h[p].tasks = f[p]->sched.d_tasks;
-    h[p].bins = f[p]->sched.d_bins;
-    h[p].stab = f[p]->sched.d_stage;
   }
   hipLaunchKernelGGL(k_zero_flags, dim3(1), dim3(64), 0, s, flags);
-  const gptq2d_status st = enqueue_upload(desc, h.data(), h.size() * sizeof(StageArgs), s);
+  const gptq2d_status st = enqueue_upload(desc, h.data(), h.size() * sizeof(BatchProb), s);
   if (st != GPTQ2D_OK) return st;
   for (int g0 = 0; g0 < count; g0 += BATCH_MAX) {
     const int cnt = std::min(BATCH_MAX, count - g0);
@@ -1215,6 +1253,7 @@ static gptq2d_status round_batched_typed(int count, const Factors* const* f, con
     for (int q = 0; q < cnt; ++q) smax = std::max(smax, f[g0 + q]->sched.stages);
     BatchLaunch bl;
     bl.desc = desc + g0;
+    bl.flags = flags;
     bl.count = cnt;
     for (int k = 0; k < smax; ++k) {
       int tot = 0;
