@@ -256,3 +256,37 @@ def test_stage_timing_is_transparent():
     for Z, Y, o in ((Z1, Y1, o1), (Z2, Y2, o2)):
         assert torch.equal(Z, Z0) and torch.equal(Y, Y0) and float(o[0]) == float(o0[0])
     f.close()
+
+
+def test_concurrent_host_threads():
+    """Two host threads, each with its own handle, stream and workspace, round
+    at the same time: each gets the result of running alone."""
+    import threading
+    probs = [wl.random_problem(300, 260, 60 + i, "f64", "wishart") for i in range(2)]
+    ref = [pr.gpu_run(p) for p in probs]
+    out = [None, None]
+    err = []
+
+    def work(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                p = probs[i]
+                f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B), stream=s)
+                for _ in range(3):
+                    Z, Y, obj = binding.round_matrix(f, pr.to_dev(p.X), stream=s)
+                s.synchronize()
+                out[i] = (Z.cpu().numpy(), float(obj.cpu()[0]))
+                f.close()
+        except Exception as e:  # reported below
+            err.append(e)
+
+    ts = [threading.Thread(target=work, args=(i,)) for i in range(2)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert not err, err
+    for i in range(2):
+        assert np.array_equal(out[i][0], ref[i]["Z"])
+        assert out[i][1] == ref[i]["obj"]
