@@ -71,6 +71,18 @@ static gptq2d_status check_device(const Factors* f) {
 
 using namespace g2d;
 
+// The error word at the head of a round workspace (single or batched), after
+// the stream has been synchronised, as a status.
+static gptq2d_status round_flags_status(const void* workspace) {
+  int flags = 0;
+  hipError_t e = hipMemcpy(&flags, workspace, sizeof(int), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+  if (flags & FLAG_NONFINITE) return fail(GPTQ2D_ERR_NONFINITE, "X held a NaN or an infinity");
+  if (flags & FLAG_OVERFLOW) return fail(GPTQ2D_ERR_OVERFLOW, "a rounded value does not fit in int32");
+  if (flags & FLAG_TIMEOUT) return fail(GPTQ2D_ERR_TIMEOUT, "a wave waited too long for its neighbour");
+  return GPTQ2D_OK;
+}
+
 extern "C" {
 
 gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
@@ -350,13 +362,7 @@ gptq2d_status gptq2d_round_check(gptq2d_factors_t f, const void* workspace, void
   if (!f || !workspace) return fail(GPTQ2D_ERR_INVALID_ARG, "handle or workspace is NULL");
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-  int flags = 0;
-  e = hipMemcpy(&flags, workspace, sizeof(int), hipMemcpyDeviceToHost);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
-  if (flags & FLAG_NONFINITE) return fail(GPTQ2D_ERR_NONFINITE, "X held a NaN or an infinity");
-  if (flags & FLAG_OVERFLOW) return fail(GPTQ2D_ERR_OVERFLOW, "a rounded value does not fit in int32");
-  if (flags & FLAG_TIMEOUT) return fail(GPTQ2D_ERR_TIMEOUT, "a wave waited too long for its neighbour");
-  return GPTQ2D_OK;
+  return round_flags_status(workspace);
 }
 
 size_t gptq2d_round_batched_workspace_size(int count, const gptq2d_factors_t* f) {
@@ -397,13 +403,7 @@ gptq2d_status gptq2d_round_batched_check(const void* workspace, void* stream) {
   if (!workspace) return fail(GPTQ2D_ERR_INVALID_ARG, "workspace is NULL");
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-  int flags = 0;
-  e = hipMemcpy(&flags, workspace, sizeof(int), hipMemcpyDeviceToHost);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
-  if (flags & FLAG_NONFINITE) return fail(GPTQ2D_ERR_NONFINITE, "X held a NaN or an infinity");
-  if (flags & FLAG_OVERFLOW) return fail(GPTQ2D_ERR_OVERFLOW, "a rounded value does not fit in int32");
-  if (flags & FLAG_TIMEOUT) return fail(GPTQ2D_ERR_TIMEOUT, "a wave waited too long for its neighbour");
-  return GPTQ2D_OK;
+  return round_flags_status(workspace);
 }
 
 gptq2d_status gptq2d_stage_timing(gptq2d_factors_t f, int enable) {
