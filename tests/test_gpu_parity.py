@@ -290,3 +290,45 @@ def test_concurrent_host_threads():
     for i in range(2):
         assert np.array_equal(out[i][0], ref[i]["Z"])
         assert out[i][1] == ref[i]["obj"]
+
+
+@pytest.mark.parametrize("reverse", [False, True])
+def test_graph_capture_replays(reverse):
+    """A whole step (factorisation, with its second stream forked and joined
+    by events, then the sweep's stage launches) captured in a HIP graph:
+    every replay, with eager work and synchronisations between the replays,
+    gives the eager result."""
+    p = wl.random_problem(520, 390, 31, "f32", "wishart")
+    A, B, X = pr.to_dev(p.A), pr.to_dev(p.B), pr.to_dev(p.X)
+    f = binding.Factors(p.m, p.n, reverse=reverse)
+    ws = f.workspace()
+    Z = torch.empty((p.m, p.n), dtype=torch.int32, device="cuda")
+    Y = torch.empty_like(X)
+    obj = torch.empty(1, dtype=torch.float64, device="cuda")
+    s = torch.cuda.Stream()
+
+    def step():
+        binding.gptq2d_factor_compute(f.handle, A, B, s)
+        binding.gptq2d_round(f.handle, X, Z, Y, obj, ws, s)
+
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.synchronize()
+    Zref, Yref, oref = Z.clone(), Y.clone(), float(obj[0])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        step()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        Z.fill_(-1)
+        Y.fill_(0.0)
+        obj.fill_(0.0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Z, Zref) and torch.equal(Y, Yref) and float(obj[0]) == oref
+        with torch.cuda.stream(s):
+            step()
+        torch.cuda.synchronize()
+    binding.gptq2d_round_check(f.handle, ws, s)
+    del g
+    f.close()
