@@ -122,3 +122,24 @@ def test_fig1_wavefronts(lib):
     assert len(offs) - 1 == 6
     waves = [[(i + 1, s - i + 1) for i in range(3) if 0 <= s - i < 4] for s in range(6)]
     assert waves[2] == [(1, 3), (2, 2), (3, 1)]
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    """Without the built HIP library the binding raises; there is no fallback."""
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", "/nonexistent/libgptq2d.so")
+    with pytest.raises(RuntimeError, match="not built"):
+        binding.load()
+
+
+def test_bench_refuses_several_gpus():
+    """bench.py measures one GPU; --gpus N > 1 exits with a message before
+    touching any device."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "exactly one GPU" in r.stderr
