@@ -265,6 +265,14 @@ gptq2d_status gptq2d_stage_time(gptq2d_factors_t f, double* total_ms, int64_t* l
 int64_t gptq2d_schedule_tasks(int m, int n, int g, int32_t* tasks, int64_t cap,
                               int32_t* offsets);
 
+/* Host-only view of which tiles each launch of the sweep rounds (Fig. 1 at
+ * the level of 64 x 64 tiles: the tiles of one tile anti-diagonal depend on
+ * none of each other, Sec. 4.2); touches no device. Launch k sweeps tile rows
+ * rows[2k] .. rows[2k+1] (host, 2*cap int32, nullable; filled for k < cap),
+ * row I at tile column k - I. Returns the number of launches MT + NT - 1, or
+ * -1 on a bad shape (1 <= m, n <= 65536) or a negative cap. */
+int64_t gptq2d_schedule_sweeps(int m, int n, int32_t* rows, int64_t cap);
+
 #ifdef __cplusplus
 }
 #endif

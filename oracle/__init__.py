@@ -21,6 +21,11 @@ This module is argument marshalling around ``oracle.c`` (plain C, fp64):
 * ``round_gptq2d``                -- Algorithm 3 (Sec. 4.2)
 * ``round_implicit``              -- Algorithm 6 (Appendix B)
 * ``objective``                   -- ||A (Z - X) B||_F^2 by definition
+* ``trajectory_values``           -- the value every entry had when it was
+                                     rounded, given all rounding errors E:
+                                     Y = X + L E U - E (Eq. Y-LEU)
+* ``trajectory_check``            -- judges a whole (Z, Y) against that
+                                     definition and the window rule
 * ``round_reverse``               -- the same rounding in reverse order (from the
                                      last row and column, the direction of YAQA,
                                      Sec. 2): Algorithm 5 on the index-reversed
@@ -281,6 +286,45 @@ def objective(X, Z, A, B) -> float:
     B = _d(B)
     m, n = X.shape
     return float(_load().orc_objective(m, n, _dp(X), _ip(Z), _dp(A), _dp(B)))
+
+
+def trajectory_values(X, L, U, E) -> np.ndarray:
+    """Corrected values of the sweep whose rounding errors are E.
+
+    After the whole sweep Z - X = L E U (Eq. Y-LEU; proof of Theorem 2). The
+    value an entry (i, j) had when it was rounded is X_ij plus the pushes of
+    every entry rounded before it, and those are exactly the entries
+    (i', j') != (i, j) with i' <= i and j' <= j (Eq. rank-one-update). That is
+    (L E U)_ij without its own term L_ii E_ij U_jj = E_ij, so
+    Y = X + L E U - E. Two dense fp64 products (a library matmul as a step),
+    which makes this the oracle's check at sizes its sweeps cannot replay."""
+    X, L, U, E = _d(X), _d(L), _d(U), _d(E)
+    m, n = X.shape
+    if L.shape != (m, m) or U.shape != (n, n) or E.shape != (m, n):
+        raise ValueError("shape mismatch")
+    return X + (L @ E) @ U - E
+
+
+def trajectory_check(X, L, U, Z, Y, tau):
+    """Judges a complete result (Z, Y) of a sweep under factors L, U against
+    the definition above: with E = Z - Y the errors the sweep made, the values
+    Y' = X + L E U - E are what the greedy trajectory rounds from, and each
+    entry must be the nearest integer to its Y' (ties to even). An entry
+    where it is not counts as a "window" entry when Y' lies within tau of the
+    half-integer between the two candidates, otherwise as a "hard" mismatch
+    (the rule of the synchronised replay). Returns (max |Y' - Y|, counts,
+    flat indices of the first hard mismatches)."""
+    Z = np.asarray(Z)
+    Y = _d(Y)
+    Yp = trajectory_values(X, L, U, Z.astype(np.float64) - Y)
+    dev = float(np.abs(Yp - Y).max()) if Yp.size else 0.0
+    Zr = np.rint(Yp)
+    off = np.flatnonzero(Zr.ravel() != Z.ravel())
+    zo = Z.ravel()[off].astype(np.float64)
+    yo = Yp.ravel()[off]
+    near = (np.abs(zo - Zr.ravel()[off]) == 1.0) & (np.abs(yo - 0.5 * (zo + Zr.ravel()[off])) <= tau)
+    counts = {"window": int(near.sum()), "hard": int((~near).sum())}
+    return dev, counts, off[~near][:64]
 
 
 def reverse_problem(X, A, B):

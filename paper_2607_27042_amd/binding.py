@@ -74,6 +74,7 @@ def load():
         "gptq2d_last_error": (ctypes.c_char_p, []),
         "gptq2d_version": (i32, []),
         "gptq2d_schedule_tasks": (i64, [i32, i32, i32, ip32, i64, ip32]),
+        "gptq2d_schedule_sweeps": (i64, [i32, i32, ip32, i64]),
         "gptq2d_stage_timing": (i32, [vp, i32]),
         "gptq2d_stage_time": (i32, [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]),
     }
@@ -104,15 +105,30 @@ def _dt(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
-def _mat(t: torch.Tensor, rows: int, cols: int, what: str):
-    if not t.is_cuda:
-        raise ValueError(f"{what} must be a device tensor")
+def _layout(t: torch.Tensor, rows: int, cols: int, what: str) -> int:
+    """Leading dimension of a rows x cols row-major view, after checking that
+    the library may read (or write) every row of it without touching memory
+    outside the tensor or another row."""
     if t.dim() != 2 or tuple(t.shape) != (rows, cols):
         raise ValueError(f"{what} must be {rows} x {cols}, got {tuple(t.shape)}")
     if t.stride(1) != 1 and cols > 1:
         raise ValueError(f"{what} must be row-major with unit column stride")
     ld = t.stride(0) if rows > 1 else cols
-    return ctypes.c_void_p(t.data_ptr()), int(max(ld, cols))
+    if rows > 1 and ld < cols:
+        # an expanded or overlapping view: rows would alias each other
+        raise ValueError(f"{what} has row stride {ld} < {cols} columns (expanded or overlapping view)")
+    # the last element the library touches must lie inside the storage
+    need = (t.storage_offset() + (rows - 1) * ld + cols) * t.element_size()
+    if need > t.untyped_storage().nbytes():
+        raise ValueError(f"{what}: rows x ld exceed the tensor's storage")
+    return int(ld)
+
+
+def _mat(t: torch.Tensor, rows: int, cols: int, what: str):
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    ld = _layout(t, rows, cols, what)
+    return ctypes.c_void_p(t.data_ptr()), ld
 
 
 def _ptr(t):
@@ -362,6 +378,19 @@ def gptq2d_schedule_tasks(m: int, n: int, g: int):
     lib.gptq2d_schedule_tasks(m, n, g, tasks.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), total,
                               offs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
     return tasks[:total], offs
+
+
+def gptq2d_schedule_sweeps(m: int, n: int):
+    """Host-only list of the tiles each sweep launch rounds: int32[S, 2] of
+    (first, last) tile row; row I of launch k is tile (I, k - I)."""
+    import numpy as np
+    lib = load()
+    total = lib.gptq2d_schedule_sweeps(m, n, None, 0)
+    if total < 0:
+        raise ValueError(gptq2d_last_error())
+    rows = np.zeros((total, 2), dtype=np.int32)
+    lib.gptq2d_schedule_sweeps(m, n, rows.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), total)
+    return rows
 
 
 # ---------------------------------------------------------------------------

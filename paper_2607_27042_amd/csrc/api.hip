@@ -475,4 +475,15 @@ int64_t gptq2d_schedule_tasks(int m, int n, int g, int32_t* tasks, int64_t cap, 
   return (int64_t)all.size();
 }
 
+int64_t gptq2d_schedule_sweeps(int m, int n, int32_t* rows, int64_t cap) {
+  if (m < 1 || n < 1 || m > 65536 || n > 65536 || cap < 0) {
+    set_error("bad shape or capacity");
+    return -1;
+  }
+  const int MT = (m + TB - 1) / TB, NTt = (n + TB - 1) / TB, S = MT + NTt - 1;
+  if (rows)
+    for (int k = 0; k < S && k < cap; ++k) stage_rows(MT, NTt, k, rows[2 * k], rows[2 * k + 1]);
+  return S;
+}
+
 }  // extern "C"

@@ -95,6 +95,13 @@ __host__ __device__ inline Workspace carve_workspace(void* base, int mp, int np,
   return w;
 }
 size_t workspace_bytes(const Factors& f);
+
+// The tiles swept by launch k of the sweep (Fig. 1 at tile level: the tile
+// anti-diagonal I + J = k): tile rows ilo .. ihi, tile (I, k - I) each.
+__host__ __device__ inline void stage_rows(int MT, int NT, int k, int& ilo, int& ihi) {
+  ilo = k - (NT - 1) > 0 ? k - (NT - 1) : 0;
+  ihi = k < MT - 1 ? k : MT - 1;
+}
 Workspace workspace_carve(const Factors& f, void* base);
 
 // status plumbing

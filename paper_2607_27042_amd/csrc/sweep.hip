@@ -532,7 +532,7 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
       const double z = rint(yv);
       if (gi < a.m && gj + j < a.n) {
         if (!isfinite(yv)) bad |= FLAG_NONFINITE;
-        else if (fabs(z) > 2147483647.0) bad |= FLAG_OVERFLOW;
+        else if (z < -2147483648.0 || z > 2147483647.0) bad |= FLAG_OVERFLOW;
         const double zc = fmin(fmax(z, -2147483648.0), 2147483647.0);
         a.Z[(int64_t)gi * a.ldz + (gj + j) * a.cstep] = isfinite(zc) ? (int32_t)zc : 0;
         if (Y) Y[(int64_t)gi * a.ldy + (gj + j) * a.cstep] = (T)yv;
@@ -781,8 +781,9 @@ __global__ __launch_bounds__(NT) void k_stage_batch(BatchLaunch bl) {
   const int k = bl.stage, lb = b - bl.off[lo];
   const int4 st = a.stab[k];
   a.stage = k;
-  a.ilo = max(0, k - (a.NT - 1));
-  a.nsweep = min(k, a.MT - 1) - a.ilo + 1;
+  int ihi;
+  stage_rows(a.MT, a.NT, k, a.ilo, ihi);
+  a.nsweep = ihi - a.ilo + 1;
   a.tasks = a.tasks ? a.tasks + st.x : nullptr;
   a.bins = a.bins ? a.bins + st.y : nullptr;
   if (lb < a.nsweep) {
@@ -1167,7 +1168,8 @@ static StageArgs stage_args(const Factors& f, const void* X, int64_t ldx, int32_
 
 // work groups of stage k of a problem: the tile sweeps beside the delivery bins
 static int stage_blocks(const Factors& f, int k) {
-  const int ilo = std::max(0, k - (f.NT - 1)), ihi = std::min(k, f.MT - 1);
+  int ilo, ihi;
+  stage_rows(f.MT, f.NT, k, ilo, ihi);
   return (ihi - ilo + 1) + (f.sched.bin_offset[k + 1] - f.sched.bin_offset[k]);
 }
 
@@ -1179,7 +1181,8 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
   hipLaunchKernelGGL(k_zero_flags, dim3(1), dim3(64), 0, s, ws.flags);
   const Schedule& S = f.sched;
   for (int k = 0; k < S.stages; ++k) {
-    const int ilo = std::max(0, k - (f.NT - 1)), ihi = std::min(k, f.MT - 1);
+    int ilo, ihi;
+    stage_rows(f.MT, f.NT, k, ilo, ihi);
     a.stage = k;
     a.ilo = ilo;
     a.nsweep = ihi - ilo + 1;

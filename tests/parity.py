@@ -91,3 +91,37 @@ def property_checks(prob, res, nprobe=2, seed=0):
         scale = np.abs(L).max() * np.abs(U).max() * np.sqrt(prob.m * prob.n) * np.abs(v).max()
         tol = 1e-9 if prob.dtype == "f64" else 1e-5
         assert np.abs(lhs - rhs).max() <= tol * scale
+
+
+def widened_run(prob, reverse=False):
+    """The F64 entry points on the exactly widened inputs of an fp32 problem:
+    the library computes in fp64 either way, so Z and the factors must be the
+    fp32 run's bit for bit, and Y comes back unrounded."""
+    X, A, B = prob.widened()
+    import paper_2607_27042_amd.workloads as wl
+    return gpu_run(wl.Problem(prob.name + "_w64", X, A, B, "f64"), reverse=reverse)
+
+
+def assert_same_run(res32, res64):
+    """An fp32 run and the F64 run on its widened inputs agree bit for bit
+    (Y up to the fp32 rounding of the returned values)."""
+    assert np.array_equal(res32["Z"], res64["Z"]), "Z differs between the F32 and the widened F64 run"
+    for k in ("L", "U", "lamL", "lamU"):
+        assert np.array_equal(res32[k], res64[k]), f"{k} differs between the F32 and F64 runs"
+    assert np.array_equal(res32["Y"].astype(np.float32), res64["Y"].astype(np.float32))
+    assert res32["obj"] == res64["obj"]
+
+
+def assert_trajectory(prob, res, dev_tol=1e-9):
+    """Every entry of a full result against the oracle's definition of the
+    trajectory (Eq. Y-LEU): with E = Z - Y, the value each entry is rounded
+    from is Y' = X + L E U - E, Y must equal Y' to dev_tol, and Z = rint(Y')
+    everywhere except window entries (within tau of a tie), at most 1e-4 of
+    all entries. res["Y"] must be the unrounded fp64 values."""
+    X = prob.X.astype(np.float64)
+    dev, c, hard = oracle.trajectory_check(X, res["L"], res["U"], res["Z"], res["Y"], TAU[prob.dtype])
+    print(f"[trajectory] {prob.name}: max |Y' - Y| = {dev:.3e}, window {c['window']}, hard {c['hard']}",
+          flush=True)
+    assert dev <= dev_tol, f"{prob.name}: |Y' - Y| = {dev:.3e}"
+    assert c["hard"] == 0, f"{prob.name}: {c['hard']} hard mismatches, first at {hard[:8]}"
+    assert c["window"] <= 1e-4 * X.size, f"{prob.name}: {c['window']} window entries"

@@ -114,14 +114,46 @@ def test_delivery_plan_is_exact(lib, m, n, g):
     _check_plan(m, n, g)
 
 
+def _read_fig1():
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "fig1_dependency_3x4.txt")
+    out = {}
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        key, *rest = line.split()
+        out[key] = rest
+    return out
+
+
 def test_fig1_wavefronts(lib):
-    """The 3 x 4 example of Fig. 1 has 6 anti-diagonal wavefronts, and the
-    4th set (s = 4, 1-based) is {(1,3), (2,2), (3,1)}; at tile level a
-    3 x 4 grid of tiles has the same structure (6 launches)."""
-    tasks, offs = binding.gptq2d_schedule_tasks(3 * 64, 4 * 64, 1)
-    assert len(offs) - 1 == 6
-    waves = [[(i + 1, s - i + 1) for i in range(3) if 0 <= s - i < 4] for s in range(6)]
-    assert waves[2] == [(1, 3), (2, 2), (3, 1)]
+    """The library's launch plan against Fig. 1 (tests/golden), read at tile
+    level on a grid of 3 x 4 tiles: as many launches as the figure has
+    wavefronts, every tile swept once, every arrow of the figure ((i, j) ->
+    (i, j+1) and (i, j) -> (i+1, j)) from an earlier launch to a later one,
+    and the red anti-diagonal I_4 swept together in one launch."""
+    g = _read_fig1()
+    m, n = int(g["shape"][0]), int(g["shape"][1])
+    rows = binding.gptq2d_schedule_sweeps(m * 64, n * 64)
+    assert len(rows) == int(g["wavefronts"][0])
+    launch = {}
+    for k, (lo, hi) in enumerate(rows):
+        for i in range(lo, hi + 1):
+            t = (i + 1, k - i + 1)  # 1-based, as in the figure
+            assert 1 <= t[1] <= n and t not in launch
+            launch[t] = k
+    assert len(launch) == m * n
+    for (i, j), k in launch.items():
+        for t in ((i, j + 1), (i + 1, j)):
+            if t in launch:
+                assert launch[t] > k, (i, j, t)
+    red = [tuple(int(v) for v in e.split(",")) for e in g["red_set"][1:]]
+    ks = {launch[t] for t in red}
+    assert len(ks) == 1
+    assert sorted(t for t, k in launch.items() if k in ks) == sorted(red)
+    # the same structure at a ragged size: tile rows never go out of range
+    rows = binding.gptq2d_schedule_sweeps(700, 130)
+    assert len(rows) == 11 + 3 - 1 and (rows[:, 0] <= rows[:, 1]).all()
 
 
 def test_missing_library_fails_loudly(monkeypatch):
@@ -143,3 +175,25 @@ def test_bench_refuses_several_gpus():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "exactly one GPU" in r.stderr
+
+
+def test_binding_refuses_aliased_or_short_views():
+    """The binding hands the library a pointer and a row stride; a view whose
+    rows alias each other (expanded, overlapping as_strided) or whose last
+    row runs past its storage is refused before any call."""
+    import torch
+    base = torch.zeros((6, 8), dtype=torch.float32)
+    assert binding._layout(base, 6, 8, "X") == 8
+    assert binding._layout(base[:, 2:7], 6, 5, "X") == 8
+    assert binding._layout(base[2:3], 1, 8, "X") == 8
+    with pytest.raises(ValueError, match="row stride"):
+        binding._layout(torch.zeros(8).expand(6, 8), 6, 8, "X")
+    with pytest.raises(ValueError, match="row stride"):
+        binding._layout(torch.zeros(20).as_strided((6, 8), (2, 1)), 6, 8, "Z")
+    short = torch.zeros(48)
+    view = short.view(6, 8)
+    short.untyped_storage().resize_(40 * 4)  # the storage shrinks under the view
+    with pytest.raises(ValueError, match="storage"):
+        binding._layout(view, 6, 8, "Y")
+    with pytest.raises(ValueError, match="unit column stride"):
+        binding._layout(base.t(), 8, 6, "X")

@@ -223,6 +223,68 @@ def test_nonfinite_input_is_reported():
     assert ei.value.status == -3
 
 
+def _with_x(p, X):
+    return wl.Problem(p.name + "_x", np.ascontiguousarray(X.astype(p.X.dtype)), p.A, p.B, p.dtype)
+
+
+@pytest.mark.parametrize("kind", ["diag", "general"])
+def test_overflow_is_reported(kind):
+    """A rounded value outside int32 is an error on both sides: one entry of
+    3e9 gives GPTQ2D_ERR_OVERFLOW on the GPU and a range error in the oracle."""
+    p = wl.random_problem(70, 130, 3, "f64", kind)
+    X = p.X.copy()
+    X[37, 101] = 3e9
+    q = _with_x(p, X)
+    print(f"[overflow] {kind}", flush=True)
+    with pytest.raises(binding.Gptq2dError) as ei:
+        pr.gpu_run(q)
+    assert ei.value.status == -7
+    Xw, A, B = q.widened()
+    L, lamL, U, lamU = oracle.factors(A, B)
+    with pytest.raises(oracle.OracleError, match="int32"):
+        oracle.round_nested(Xw, L, U)
+
+
+def test_int32_ends_are_accepted():
+    """-2^31 and 2^31 - 1 are valid results (diagonal bases: Y = X exactly)."""
+    p = wl.random_problem(65, 70, 4, "f64", "diag")
+    X = p.X.copy()
+    X[0, 0] = -2147483648.0
+    X[64, 69] = 2147483647.4
+    X[10, 3] = -2147483648.4
+    res = pr.gpu_run(_with_x(p, X))
+    assert res["Z"][0, 0] == -2147483648 and res["Z"][64, 69] == 2147483647
+    assert res["Z"][10, 3] == -2147483648
+    assert np.array_equal(res["Z"], np.rint(X).astype(np.int32))
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_exact_ties(dtype):
+    """Exact half-integer ties (Theorem 1 only asks for a deterministic rule;
+    both sides break them to even). With diagonal bases Y = X exactly, so
+    every entry of an X on the half-integer grid is a tie and Z is the
+    half-even rounding of X. Under a general basis X on a grid of halves puts
+    a tie at least at the first entry, and the oracle replays the sweep."""
+    rng = np.random.default_rng(99)
+    m, n = 131, 150
+    p = wl.random_problem(m, n, 12, dtype, "diag")
+    X = rng.integers(-40, 40, size=(m, n)) + 0.5
+    res = pr.gpu_run(_with_x(p, X))
+    assert np.array_equal(res["Z"], np.rint(X).astype(np.int32))
+    assert np.array_equal(res["Y"], X)
+    g = wl.random_problem(m, n, 13, dtype, "general")
+    Xg = rng.integers(-80, 80, size=(m, n)) / 2.0
+    Xg[0, 0] = 2.5
+    q = _with_x(g, Xg)
+    res = pr.gpu_run(q)
+    assert res["Z"][0, 0] == 2
+    Zo, Yo, c, hard = pr.replay(q, res["L"], res["U"], res["Z"])
+    pr.assert_replay_pass(q, c, hard, m * n)
+    L, lamL, U, lamU = oracle.factors(*q.widened()[1:])
+    Zo3, Yo3, c3, hard3 = pr.replay(q, L, U, res["Z"])
+    pr.assert_replay_pass(q, c3, hard3, m * n)
+
+
 def test_argument_errors():
     p = wl.random_problem(70, 50, 9, "f64", "wishart")
     f = binding.Factors.from_bases(pr.to_dev(p.A), pr.to_dev(p.B))

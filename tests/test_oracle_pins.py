@@ -464,3 +464,153 @@ def test_fig1_dependency_graph():
                     assert Zp[i - 1, j - 1] == Z0[i - 1, j - 1]
     # the feedback does reach later entries (a sweep without pushes would not)
     assert changed_somewhere
+
+
+# --------------------------------------------------------------------------
+# Algorithm 1 on its own (round_1d)
+# --------------------------------------------------------------------------
+
+def _greedy_1d_bruteforce(x, Q):
+    """Babai's greedy over x in index order under the metric r^T Q r: each
+    coordinate is the integer minimising the objective with the earlier ones
+    fixed and the later ones free (ties to even)."""
+    d = len(x)
+    z = np.zeros(d)
+    for k in range(d):
+        a, b = np.arange(k + 1), np.arange(k + 1, d)
+        S = Q[np.ix_(a, a)]
+        if len(b):
+            S = S - Q[np.ix_(a, b)] @ np.linalg.solve(Q[np.ix_(b, b)], Q[np.ix_(b, a)])
+        r_prev = z[:k] - x[:k]
+        cont = x[k] - (S[k, :k] @ r_prev) / S[k, k]
+        cands = np.arange(np.floor(cont) - 2, np.ceil(cont) + 3)
+        vals = np.array([np.append(r_prev, t - x[k]) @ S @ np.append(r_prev, t - x[k]) for t in cands])
+        best = cands[np.isclose(vals, vals.min(), rtol=1e-12, atol=1e-12)]
+        z[k] = best[0] if len(best) == 1 else best[best % 2 == 0][0]
+    return z.astype(np.int32)
+
+
+@pytest.mark.parametrize("d", [1, 2, 4, 7])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_round_1d_bruteforce(d, seed):
+    """Algorithm 1 with GPTQ's feedback factor (from numpy's Cholesky of the
+    inverse metric, not the oracle's LDL) is Babai's greedy search."""
+    rng = np.random.default_rng(500 + 10 * d + seed)
+    W = rng.standard_normal((2 * d + 2, d))
+    Q = W.T @ W + 0.3 * np.eye(d)
+    R = np.linalg.cholesky(np.linalg.inv(Q)).T  # upper, Q^{-1} = R^T R
+    F = R.T / np.diag(R)[None, :]
+    x = 2.5 * rng.standard_normal(d)
+    z, y, c, _ = oracle.round_1d(x, F)
+    assert np.array_equal(z, _greedy_1d_bruteforce(x, Q))
+    assert c == {"window": 0, "hard": 0, "range": 0}
+    assert np.abs(y - z).max() <= 0.5
+
+
+def test_round_1d_ties_to_even():
+    x = np.array([0.5, 1.5, 2.5, -0.5, -1.5, -2.5])
+    z, y, _, _ = oracle.round_1d(x, np.eye(6))
+    assert z.tolist() == [0, 2, 2, 0, -2, -2]
+    assert np.array_equal(y, x)
+
+
+@pytest.mark.parametrize("m,n", [(6, 3), (13, 5)])
+def test_round_1d_is_the_column_sweep_under_right_identity(m, n):
+    """B = I: every column of the two-sided sweep is Algorithm 1 on that
+    column under L (Sec. 4.1: U = I removes all rightward feedback)."""
+    X, A, B = _prob(m, n, 71, "identity_right")
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    for j in range(n):
+        z, y, _, _ = oracle.round_1d(X[:, j], L)
+        assert np.array_equal(z, Z[:, j])
+        np.testing.assert_allclose(y, Y[:, j], rtol=0, atol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# The trajectory by its definition: Y = X + L E U - E (Eq. Y-LEU)
+# --------------------------------------------------------------------------
+
+def _trajectory_bruteforce(X, L, U, E):
+    """Y'_ij = X_ij plus the push of every entry rounded before (i, j), summed
+    entry by entry over (i', j') != (i, j) with i' <= i, j' <= j."""
+    m, n = X.shape
+    Y = np.array(X, dtype=np.float64)
+    for i in range(m):
+        for j in range(n):
+            s = 0.0
+            for i2 in range(i + 1):
+                for j2 in range(j + 1):
+                    if (i2, j2) != (i, j):
+                        s += L[i, i2] * E[i2, j2] * U[j2, j]
+            Y[i, j] += s
+    return Y
+
+
+@pytest.mark.parametrize("m,n", [(1, 1), (1, 6), (5, 1), (4, 7), (9, 5)])
+def test_trajectory_values_bruteforce(m, n):
+    rng = np.random.default_rng(300 + 10 * m + n)
+    L = np.tril(rng.standard_normal((m, m)), -1) + np.eye(m)
+    U = np.triu(rng.standard_normal((n, n)), 1) + np.eye(n)
+    X = 3 * rng.standard_normal((m, n))
+    E = rng.uniform(-0.5, 0.5, (m, n))
+    np.testing.assert_allclose(oracle.trajectory_values(X, L, U, E), _trajectory_bruteforce(X, L, U, E),
+                               rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("m,n,kind", [(7, 7, "wishart"), (16, 11, "general"), (24, 24, "lower"),
+                                      (5, 30, "wishart")])
+def test_trajectory_values_reproduce_the_sweeps(m, n, kind):
+    """The errors of a sweep give back the values it rounded from: for the
+    nested sweep (Algorithm 5) and, where it is affordable, for the quartic
+    sweep over vec(X), which never sees L or U."""
+    X, A, B = _prob(m, n, 61, kind)
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    scale = max(1.0, float(np.abs(X).max()))
+    np.testing.assert_allclose(oracle.trajectory_values(X, L, U, Z - Y), Y, rtol=0, atol=1e-10 * scale)
+    dev, c, hard = oracle.trajectory_check(X, L, U, Z, Y, 0.0)
+    assert c == {"window": 0, "hard": 0} and dev <= 1e-10 * scale
+    if m * n <= 256:
+        Zq, Yq, _, _ = oracle.round_quartic(X, A, B)
+        np.testing.assert_allclose(oracle.trajectory_values(X, L, U, Zq - Yq), Yq, rtol=0,
+                                   atol=1e-9 * scale)
+
+
+def test_trajectory_check_counts():
+    """A flipped decision far from a tie is a hard mismatch at that entry
+    (its own value does not include its own error); a flip of an entry within
+    tau of a tie is a window entry."""
+    X, A, B = _prob(8, 9, 12, "wishart")
+    L, _, U, _ = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    k = int(np.argmin(np.abs(np.abs(Z - Y) - 0.5) * -1))  # the entry farthest from a tie
+    Zb = Z.copy().ravel()
+    Zb[k] += 1
+    dev, c, hard = oracle.trajectory_check(X, L, U, Zb.reshape(Z.shape), Y, 1e-6)
+    assert c["hard"] >= 1 and hard[0] == k
+    Xt = np.array([[0.5 + 1e-9]])
+    one = np.eye(1)
+    for tau, kind in ((1e-6, "window"), (1e-12, "hard")):
+        dev, c, hard = oracle.trajectory_check(Xt, one, one, np.array([[0]]), Xt, tau)
+        assert c[kind] == 1 and sum(c.values()) == 1
+
+
+# --------------------------------------------------------------------------
+# Range of Z (int32)
+# --------------------------------------------------------------------------
+
+def test_int32_range_is_enforced():
+    """Z is stored as int32: -2^31 and 2^31 - 1 are accepted, one step beyond
+    either end is a range error."""
+    one = np.eye(1)
+    for x, z in ((-2147483648.0, -2147483648), (2147483647.4, 2147483647), (-2147483648.4, -2147483648)):
+        Z, _, c, _ = oracle.round_nested(np.array([[x]]), one, one)
+        assert int(Z[0, 0]) == z and c["range"] == 0
+    for x in (2147483647.6, -2147483648.6, 3e9):
+        with pytest.raises(oracle.OracleError, match="int32"):
+            oracle.round_nested(np.array([[x]]), one, one)
+    X = np.zeros((3, 4))
+    X[1, 2] = 3e9
+    with pytest.raises(oracle.OracleError, match="int32"):
+        oracle.round_nested(X, np.eye(3), np.eye(4))
