@@ -179,6 +179,27 @@ gptq2d_status gptq2d_round(gptq2d_factors_t f, gptq2d_dtype dt, const void* X, i
  * last gptq2d_round that used `workspace` met one, OK otherwise. */
 gptq2d_status gptq2d_round_check(gptq2d_factors_t f, const void* workspace, void* stream);
 
+/* gptq2d_round for callers that cannot allocate (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same kernels and
+ * results as gptq2d_round(f, dt, X, ldx, Z, ldz, Y, ldy, objective, ...), but
+ * the workspace is a fixed 64 MiB array of device memory inside the library
+ * (one per device, held from the first use on that device until the process
+ * ends), so the caller passes no workspace and the call allocates nothing.
+ *   status_word (required, device int32, owned by the caller): the error bits
+ *       of this call; gptq2d_round_check(f, status_word, stream) turns them
+ *       into NONFINITE, OVERFLOW or TIMEOUT as for gptq2d_round.
+ * Limit: gptq2d_round_workspace_size(f) <= 64 MiB, about 4 x 8 bytes per
+ * entry of X padded to multiples of 64 (e.g. up to 1408 x 1408 or 1024 x
+ * 2048); a larger problem returns WORKSPACE with the sizes in the message.
+ * All calls on one device share that device's array: calls that overlap in
+ * time on one device (two streams, two threads) race and give wrong results;
+ * calls in one stream order are safe, each overwrites what the last one
+ * left. Stage-launch timing (gptq2d_stage_timing) is ignored. Errors:
+ * INVALID_ARG, WORKSPACE, HIP. */
+gptq2d_status gptq2d_round_noalloc(gptq2d_factors_t f, gptq2d_dtype dt, const void* X, int64_t ldx,
+                                   int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,
+                                   int32_t* status_word, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Batched rounding: many independent problems (the layers of a model, Sec. 6)
  * in common launches. Stage k of every problem runs in one launch, so small

@@ -67,6 +67,7 @@ def load():
         "gptq2d_round_workspace_size": (sz, [vp]),
         "gptq2d_round": (i32, [vp, i32, vp, i64, vp, i64, vp, i64, vp, vp, sz, vp]),
         "gptq2d_round_check": (i32, [vp, vp, vp]),
+        "gptq2d_round_noalloc": (i32, [vp, i32, vp, i64, vp, i64, vp, i64, vp, vp, vp]),
         "gptq2d_round_batched_workspace_size": (sz, [i32, vp]),
         "gptq2d_round_batched": (i32, [i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "gptq2d_round_batched_check": (i32, [vp, vp]),
@@ -283,6 +284,30 @@ def gptq2d_round(h: int, X: torch.Tensor, Z: torch.Tensor, Y, objective, workspa
     _check(load().gptq2d_round(ctypes.c_void_p(h), _dt(X), px, ldx, pz, ldz, py, ldy, _ptr(objective),
                                _ptr(workspace), workspace.numel() * workspace.element_size(),
                                _stream(stream)), "gptq2d_round")
+
+
+def gptq2d_round_noalloc(h: int, X: torch.Tensor, Z: torch.Tensor, Y, objective, status_word: torch.Tensor,
+                         stream=None) -> None:
+    """gptq2d_round with the library's own fixed workspace; status_word is a
+    one-element int32 device tensor (check it with gptq2d_round_check)."""
+    m, n = gptq2d_factors_shape(h)
+    px, ldx = _mat(X, m, n, "X")
+    if Z.dtype != torch.int32:
+        raise TypeError("Z must be int32")
+    pz, ldz = _mat(Z, m, n, "Z")
+    if Y is not None:
+        if Y.dtype != X.dtype:
+            raise TypeError("Y must have X's dtype")
+        py, ldy = _mat(Y, m, n, "Y")
+    else:
+        py, ldy = ctypes.c_void_p(0), n
+    if objective is not None and (objective.dtype != torch.float64 or not objective.is_cuda):
+        raise TypeError("objective must be a float64 device tensor")
+    if status_word.dtype != torch.int32 or not status_word.is_cuda or status_word.numel() < 1:
+        raise TypeError("status_word must be an int32 device tensor")
+    _check(load().gptq2d_round_noalloc(ctypes.c_void_p(h), _dt(X), px, ldx, pz, ldz, py, ldy,
+                                       _ptr(objective), _ptr(status_word), _stream(stream)),
+           "gptq2d_round_noalloc")
 
 
 def gptq2d_round_check(h: int, workspace: torch.Tensor, stream=None) -> None:

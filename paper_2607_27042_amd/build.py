@@ -8,7 +8,7 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SRC = [os.path.join(PKG, "csrc", f) for f in ("api.hip", "factor.hip", "sweep.hip")]
+SRC = [os.path.join(PKG, "csrc", f) for f in ("api.hip", "factor.hip", "sweep.hip", "noalloc.hip")]
 HDR = [os.path.join(PKG, "csrc", f) for f in ("device.hpp", "internal.hpp")] + [
     os.path.join(ROOT, "include", "gptq2d.h")]
 LIB = os.path.join(PKG, "lib", "libgptq2d.so")

@@ -10,8 +10,6 @@
 #include "device.hpp"
 #include "internal.hpp"
 
-struct gptq2d_factors_s : g2d::Factors {};
-
 namespace g2d {
 
 static thread_local std::string g_last_error;
@@ -58,12 +56,22 @@ static int env_int(const char* name, int def) {
   return atoi(v);
 }
 
-static gptq2d_status check_device(const Factors* f) {
+gptq2d_status check_device(const Factors* f) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   if (dev != f->device)
     return fail(GPTQ2D_ERR_INVALID_ARG, "the current device is not the device of the handle");
+  return GPTQ2D_OK;
+}
+
+gptq2d_status check_round_args(const Factors* f, gptq2d_dtype dt, const void* X, int64_t ldx,
+                               const int32_t* Z, int64_t ldz, const void* Y, int64_t ldy) {
+  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
+  if (dt != GPTQ2D_F32 && dt != GPTQ2D_F64) return fail(GPTQ2D_ERR_INVALID_ARG, "bad dtype");
+  if (!X || !Z) return fail(GPTQ2D_ERR_INVALID_ARG, "X or Z is NULL");
+  if (ldx < f->n || ldz < f->n || (Y && ldy < f->n))
+    return fail(GPTQ2D_ERR_INVALID_ARG, "leading dimension too small");
   return GPTQ2D_OK;
 }
 
@@ -343,11 +351,8 @@ size_t gptq2d_round_workspace_size(gptq2d_factors_t f) { return f ? workspace_by
 gptq2d_status gptq2d_round(gptq2d_factors_t f, gptq2d_dtype dt, const void* X, int64_t ldx,
                            int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,
                            void* workspace, size_t ws_bytes, void* stream) {
-  if (!f) return fail(GPTQ2D_ERR_INVALID_ARG, "handle is NULL");
-  if (dt != GPTQ2D_F32 && dt != GPTQ2D_F64) return fail(GPTQ2D_ERR_INVALID_ARG, "bad dtype");
-  if (!X || !Z) return fail(GPTQ2D_ERR_INVALID_ARG, "X or Z is NULL");
-  if (ldx < f->n || ldz < f->n || (Y && ldy < f->n))
-    return fail(GPTQ2D_ERR_INVALID_ARG, "leading dimension too small");
+  const gptq2d_status sa = check_round_args(f, dt, X, ldx, Z, ldz, Y, ldy);
+  if (sa != GPTQ2D_OK) return sa;
   if (!workspace || ws_bytes < workspace_bytes(*f))
     return fail(GPTQ2D_ERR_WORKSPACE, "workspace missing or smaller than gptq2d_round_workspace_size()");
   if (((uintptr_t)workspace) % 256 != 0)

@@ -107,6 +107,11 @@ Workspace workspace_carve(const Factors& f, void* base);
 // status plumbing
 void set_error(const std::string& msg);
 gptq2d_status hip_fail(hipError_t e, const char* what);
+// the handle's device is the current one
+gptq2d_status check_device(const Factors* f);
+// the arguments gptq2d_round checks before its workspace
+gptq2d_status check_round_args(const Factors* f, gptq2d_dtype dt, const void* X, int64_t ldx,
+                               const int32_t* Z, int64_t ldz, const void* Y, int64_t ldy);
 
 // factorisation launches (enqueued on stream, no synchronisation)
 // doubles of scratch for the Gram tiles split between work groups
@@ -140,9 +145,11 @@ gptq2d_status pack_bins(int MT, int NT, int units, std::vector<int4>& all,
                         std::vector<int>& bin_offset);
 gptq2d_status build_schedule(Factors& f, int g);
 void free_schedule(Schedule& s);
+// allow_timing = false: no stage-launch timing even if the handle asks for it
+// (timing creates HIP events on first use)
 gptq2d_status launch_round(const Factors& f, gptq2d_dtype dt, const void* X, int64_t ldx,
                            int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,
-                           const Workspace& ws, hipStream_t s);
+                           const Workspace& ws, hipStream_t s, bool allow_timing = true);
 
 // batched rounding: `count` problems, one workspace region each, in common
 // stage launches (workspace layout in sweep.hip)
@@ -153,3 +160,6 @@ gptq2d_status launch_round_batched(int count, const Factors* const* f, gptq2d_dt
                                    double* objective, void* workspace, hipStream_t s);
 
 }  // namespace g2d
+
+// the opaque handle of the C ABI is the factor record itself
+struct gptq2d_factors_s : g2d::Factors {};

@@ -1176,7 +1176,7 @@ static int stage_blocks(const Factors& f, int k) {
 template <typename T>
 static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, int32_t* Z,
                                  int64_t ldz, void* Y, int64_t ldy, double* objective,
-                                 const Workspace& ws, hipStream_t s) {
+                                 const Workspace& ws, hipStream_t s, bool allow_timing) {
   StageArgs a = stage_args<T>(f, X, ldx, Z, ldz, Y, ldy, ws);
   hipLaunchKernelGGL(k_zero_flags, dim3(1), dim3(64), 0, s, ws.flags);
   const Schedule& S = f.sched;
@@ -1190,7 +1190,7 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
     a.tasks = S.d_tasks ? S.d_tasks + S.offset[k] : nullptr;
     a.bins = S.d_bins ? S.d_bins + S.bin_offset[k] : nullptr;
     hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (f.stage_timing) {
+    if (f.stage_timing && allow_timing) {
       while (f.stage_ev.size() < f.stage_ev_used + 2) {
         hipEvent_t ev;
         hipError_t e = hipEventCreate(&ev);
@@ -1214,9 +1214,9 @@ static gptq2d_status round_typed(const Factors& f, const void* X, int64_t ldx, i
 
 gptq2d_status launch_round(const Factors& f, gptq2d_dtype dt, const void* X, int64_t ldx,
                            int32_t* Z, int64_t ldz, void* Y, int64_t ldy, double* objective,
-                           const Workspace& ws, hipStream_t s) {
-  if (dt == GPTQ2D_F32) return round_typed<float>(f, X, ldx, Z, ldz, Y, ldy, objective, ws, s);
-  return round_typed<double>(f, X, ldx, Z, ldz, Y, ldy, objective, ws, s);
+                           const Workspace& ws, hipStream_t s, bool allow_timing) {
+  if (dt == GPTQ2D_F32) return round_typed<float>(f, X, ldx, Z, ldz, Y, ldy, objective, ws, s, allow_timing);
+  return round_typed<double>(f, X, ldx, Z, ldz, Y, ldy, objective, ws, s, allow_timing);
 }
 
 // Workspace of a batch: the batch's error flags (256 bytes), the problems'
