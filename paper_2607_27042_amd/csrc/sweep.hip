@@ -353,27 +353,8 @@ __device__ void run_bin(const StageArgs& a, int4 bin, TaskSmem& sm) {
 }
 
 // acc += A (16 x K) B (K x 16) on MFMA, both operands row-major in LDS with
-// row strides lda, ldb; K a multiple of 16 (0 allowed). One wave. Each
-// 16-deep chunk issues its eight operand loads before its four MFMAs.
-__device__ __forceinline__ void mma16(d4& acc, const double* pa, int lda, const double* pb, int ldb,
-                                      int K) {
-  const int l = threadIdx.x & 63;
-  const double* qa = pa + (l & 15) * lda + (l >> 4);
-  const double* qb = pb + (l >> 4) * ldb + (l & 15);
-#pragma unroll 1
-  for (int k0 = 0; k0 < K; k0 += 16) {
-    double av[4], bv[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      av[s] = qa[k0 + 4 * s];
-      bv[s] = qb[(k0 + 4 * s) * ldb];
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[s], bv[s], acc, 0, 0, 0);
-  }
-}
-
-// The same with a compile-time depth: every operand load is issued first.
+// row strides lda, ldb; K a compile-time multiple of 4: every operand load is
+// issued first.
 template <int K>
 __device__ __forceinline__ void mma16k(d4& acc, const double* pa, int lda, const double* pb, int ldb) {
   if constexpr (K > 0) {
@@ -397,8 +378,44 @@ struct Band {
   double* Et;      // the tile's E (R order) and C (S order)
   double* Ct;
   double l10;      // L[br+1][br]
+  double u01[4];   // U[uc+2q][uc+2q+1] of sub-tile c (uc = 16 c)
   double dl[2];    // 1 / lamL of the lane's two rows
+  bool interior;   // the whole tile lies inside the matrix
+  int32_t* zr[2];  // Z and Y at the lane's two rows, column 2q of the tile
+  void* yr[2];
 };
+
+// Bounded wait until a band's release counter reaches v (workgroup-scope
+// acquire); a wait that runs out raises the time-out flag instead of hanging.
+__device__ __forceinline__ void wait_band(const int* done, int v, int& bad) {
+  int spins = 0;
+  while (__hip_atomic_load(done, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < v) {
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins > (1 << 22)) {
+      bad |= FLAG_TIMEOUT;
+      break;
+    }
+  }
+}
+
+// acc += A (16 x K) B (K x 16) on MFMA for a K that is a multiple of 16 known
+// only at run time (the wave's band index); operands row-major in LDS.
+__device__ __forceinline__ void mma16(d4& acc, const double* pa, int lda, const double* pb, int ldb, int K) {
+  const int l = threadIdx.x & 63;
+  const double* qa = pa + (l & 15) * lda + (l >> 4);
+  const double* qb = pb + (l >> 4) * ldb + (l & 15);
+#pragma unroll 1
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    double av[4], bv[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      av[s] = qa[k0 + 4 * s];
+      bv[s] = qb[(k0 + 4 * s) * ldb];
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[s], bv[s], acc, 0, 0, 0);
+  }
+}
 
 // Sub-tile (w, C) of the band: wait for the band above, add the in-tile
 // feedback of the finished sub-tiles above and to the left, run Algorithm 3
@@ -410,16 +427,7 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
   const int w = b.w, l = b.l, p = b.p, q = b.q, br = b.br;
   constexpr int uc = SS * C;
   // the band above must have finished sub-tile C
-  if (w > 0) {
-    int spins = 0;
-    while (__hip_atomic_load(&sm.done[w - 1], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) <= C) {
-      __builtin_amdgcn_s_sleep(1);
-      if (++spins > (1 << 22)) {
-        bad |= FLAG_TIMEOUT;
-        break;
-      }
-    }
-  }
+  if (w > 0) wait_band(&sm.done[w - 1], C + 1, bad);
   // feedback from the finished sub-tiles above (same column) and to the left
   // (same band) inside this tile
   {
@@ -451,29 +459,41 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
   // anti-diagonals). In every step each lane first adds the feedback of the
   // blocks finished in the step before that lie above it in its block column
   // (errors through L, Alg. 3 push down) or left of it in its block row (C
-  // through U, push right); other source positions get a zero weight (the
-  // zero column of Ls, the zero rows of Us) and a zero operand.
+  // through U, push right). Those source blocks are read unconditionally
+  // (every LDS word they can reach holds a finite value); a source that does
+  // not feed the lane gets a zero weight: the zero column of Ls, the zero rows
+  // of Us, or, for the block on the lane's own diagonal, the 2 x 2 diagonal
+  // blocks of Ls and Us, which hold zeros during the sweep (their one
+  // off-diagonal entry is kept in a register).
   // So a lane's accumulators stop changing after its own step, and every
   // lane runs the rounding chain in every step without a branch: before its
   // step it publishes finite placeholders that nobody reads with a nonzero
   // weight, from its step on the final E and C of its block (read back by
   // the same wave in the next step: LDS is in order within a wave, no
   // barrier). The results of the last step are every lane's final values.
-  const double u01 = sm.Us[uc + 2 * q][uc + 2 * q + 1];
+  const double u01 = b.u01[C];
+  const double l10 = b.l10;
+  const double ul = u01 * l10;
   double* const eown = &sm.x.t.Et[br][uc + 2 * q];
   double* const cown = &sm.x.t.Ct[br][uc + 2 * q];
-  const double* const zpad = &sm.Us[TB][0];  // two zero rows: the unused sources
-  double yf[2][2], cf[2][2];
+  // sources at step k: E rows 16 w + 2 (k-1-q) .. +1 at the lane's columns,
+  // C columns uc + 2 (k-1-p) .. +1 at the lane's rows (a per-lane base plus
+  // a constant offset: no address arithmetic in the steps)
+  const double* const pe0 = &sm.x.t.Et[0][0] + (SS * w - 2 - 2 * q) * TP + uc + 2 * q;
+  const double* const pc0 = &sm.x.t.Ct[0][0] + br * TP + uc - 2 - 2 * p;
+  const double* const pl0 = &sm.Ls[br][0];
+  const double* const pu0 = &sm.Us[0][0] + uc + 2 * q;
+  const int lcol = SS * w - 2 - 2 * q;  // weight column of step k: lcol + 2 k
+  const int urow = uc - 2 - 2 * p;      // weight row of step k: urow + 2 k
+  double yf[2][2], cf[2][2], ef[2][2];
 #pragma unroll
   for (int k = 0; k < SS - 1; ++k) {
     const bool vr = (unsigned)(k - 1 - q) < (unsigned)p;  // source block row k-1-q above
     const bool vc = (unsigned)(k - 1 - p) < (unsigned)q;  // source block column k-1-p left
-    const int er = SS * w + 2 * (k - 1 - q);                // its tile row
-    const int cc = uc + 2 * (k - 1 - p);                    // its tile column
-    const double* pe = vr ? &sm.x.t.Et[0][0] + er * TP + uc + 2 * q : zpad;
-    const double* pl = &sm.Ls[br][0] + (vr ? er : TB);
-    const double* pc = vc ? &sm.x.t.Ct[0][0] + br * TP + cc : zpad;
-    const double* pu = &sm.Us[0][0] + (vc ? cc : TB) * TP + uc + 2 * q;
+    const double* pe = pe0 + 2 * k * TP;
+    const double* pc = pc0 + 2 * k;
+    const double* pl = pl0 + (vr ? lcol + 2 * k : TB);
+    const double* pu = pu0 + (vc ? urow + 2 * k : TB) * TP;
     const double2 e0 = *reinterpret_cast<const double2*>(pe);
     const double2 e1 = *reinterpret_cast<const double2*>(pe + TP);
     const double2 l0 = *reinterpret_cast<const double2*>(pl);
@@ -490,20 +510,30 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
     Rc[0][1] = fma(c0.y, v1.y, fma(c0.x, v0.y, Rc[0][1]));
     Rc[1][0] = fma(c1.y, v1.x, fma(c1.x, v0.x, Rc[1][0]));
     Rc[1][1] = fma(c1.y, v1.y, fma(c1.x, v0.y, Rc[1][1]));
+    // The in-block chain, with every term that does not wait for this step's
+    // errors formed first. With D, R the accumulated feedback and
+    // C = D + E (L has a unit diagonal):
+    //   y00 = R00 + D00
+    //   y01 = R01 + D01 + u01 C00          = k01 + u01 e00
+    //   y10 = R10 + D10 + l10 e00          = k10 + l10 e00
+    //   y11 = R11 + D11 + l10 e01 + u01 C10
+    //       = k11 + u01 l10 e00 + l10 e01 + u01 e10
     const double y00 = Rc[0][0] + Dc[0][0];
+    const double k01 = fma(Dc[0][0], u01, Rc[0][1] + Dc[0][1]);
+    const double k10 = Rc[1][0] + Dc[1][0];
+    const double k11 = fma(Dc[1][0], u01, Rc[1][1] + Dc[1][1]);
     const double e00 = rint(y00) - y00;
-    const double c00 = Dc[0][0] + e00;
-    const double d10 = fma(b.l10, e00, Dc[1][0]);
-    const double y01 = fma(c00, u01, Rc[0][1]) + Dc[0][1];
+    const double y01 = fma(e00, u01, k01);
+    const double y10 = fma(e00, l10, k10);
+    const double m11 = fma(e00, ul, k11);
     const double e01 = rint(y01) - y01;
-    const double c01 = Dc[0][1] + e01;
-    const double y10 = Rc[1][0] + d10;
     const double e10 = rint(y10) - y10;
-    const double c10 = d10 + e10;
-    const double d11 = fma(b.l10, e01, Dc[1][1]);
-    const double y11 = fma(c10, u01, Rc[1][1]) + d11;
+    const double y11 = fma(e10, u01, fma(e01, l10, m11));
     const double e11 = rint(y11) - y11;
-    const double c11 = d11 + e11;
+    const double c00 = Dc[0][0] + e00;
+    const double c01 = Dc[0][1] + e01;
+    const double c10 = fma(l10, e00, Dc[1][0]) + e10;
+    const double c11 = fma(l10, e01, Dc[1][1]) + e11;
     *reinterpret_cast<double2*>(eown) = double2{e00, e01};
     *reinterpret_cast<double2*>(eown + TP) = double2{e10, e11};
     *reinterpret_cast<double2*>(cown) = double2{c00, c01};
@@ -511,32 +541,61 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
     if (k == SS - 2) {
       yf[0][0] = y00; yf[0][1] = y01; yf[1][0] = y10; yf[1][1] = y11;
       cf[0][0] = c00; cf[0][1] = c01; cf[1][0] = c10; cf[1][1] = c11;
+      ef[0][0] = e00; ef[0][1] = e01; ef[1][0] = e10; ef[1][1] = e11;
     }
   }
 
   // hand-off to the band below, then the global outputs
   __hip_atomic_store(&sm.done[w], C + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-  T* Y = (T*)a.Y;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int gi = b.gi0 + br + i;
-    const int gj = b.gj0 + uc + 2 * q;
-    double ev[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) ev[j] = rint(yf[i][j]) - yf[i][j];
-    *reinterpret_cast<double2*>(b.Et + r_idx(br + i, uc + 2 * q)) = double2{ev[0], ev[1]};
+    *reinterpret_cast<double2*>(b.Et + r_idx(br + i, uc + 2 * q)) = double2{ef[i][0], ef[i][1]};
     *reinterpret_cast<double2*>(b.Ct + s_idx(br + i, uc + 2 * q)) = double2{cf[i][0], cf[i][1]};
+  }
+  const int64_t cs = a.cstep;
+  if (b.interior) {
+    // every entry of the tile lies inside the matrix: no bounds checks, and
+    // the range check folded into one test per entry (NaN fails it too)
+    bool ok = true;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const double yv = yf[i][j];
-      const double z = rint(yv);
-      if (gi < a.m && gj + j < a.n) {
-        if (!isfinite(yv)) bad |= FLAG_NONFINITE;
-        else if (z < -2147483648.0 || z > 2147483647.0) bad |= FLAG_OVERFLOW;
-        const double zc = fmin(fmax(z, -2147483648.0), 2147483647.0);
-        a.Z[(int64_t)gi * a.ldz + (gj + j) * a.cstep] = isfinite(zc) ? (int32_t)zc : 0;
-        if (Y) Y[(int64_t)gi * a.ldy + (gj + j) * a.cstep] = (T)yv;
-        part += ev[j] * ev[j] * b.dl[i] * dc[j];
+    for (int i = 0; i < 2; ++i) {
+      int32_t* zr = b.zr[i] + uc * cs;
+      T* yr = b.yr[i] ? (T*)b.yr[i] + uc * cs : nullptr;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const double yv = yf[i][j];
+        ok = ok && yv >= -2147483648.5 && yv < 2147483647.5;
+        const double zc = fmin(fmax(rint(yv), -2147483648.0), 2147483647.0);
+        zr[j * cs] = (int32_t)zc;
+        if (yr) yr[j * cs] = (T)yv;
+        part = fma(ef[i][j] * ef[i][j], b.dl[i] * dc[j], part);
+      }
+    }
+    if (!ok) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) bad |= isfinite(yf[i][j]) ? 0 : FLAG_NONFINITE;
+      if (!(bad & FLAG_NONFINITE)) bad |= FLAG_OVERFLOW;
+    }
+  } else {
+    T* Y = (T*)a.Y;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int gi = b.gi0 + br + i;
+      const int gj = b.gj0 + uc + 2 * q;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const double yv = yf[i][j];
+        const double z = rint(yv);
+        if (gi < a.m && gj + j < a.n) {
+          if (!isfinite(yv)) bad |= FLAG_NONFINITE;
+          else if (z < -2147483648.0 || z > 2147483647.0) bad |= FLAG_OVERFLOW;
+          const double zc = fmin(fmax(z, -2147483648.0), 2147483647.0);
+          a.Z[(int64_t)gi * a.ldz + (gj + j) * cs] = isfinite(zc) ? (int32_t)zc : 0;
+          if (Y) Y[(int64_t)gi * a.ldy + (gj + j) * cs] = (T)yv;
+          part = fma(ef[i][j] * ef[i][j], b.dl[i] * dc[j], part);
+        }
       }
     }
   }
@@ -573,6 +632,11 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
     load_blk_s(a.C + tile_off(I, J - 1, a.NT), gc);
     load_blk(a.U + tile_off(J - 1, J, a.NT), TB, gd);
   }
+  // the off-diagonal entries of the lane's 2 x 2 diagonal factor blocks
+  const double l10v = a.L[tile_off(I, I, a.MT) + s_idx(br + 1, br)];
+  double u01v[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) u01v[c] = a.U[tile_off(J, J, a.NT) + r_idx(SS * c + 2 * q, SS * c + 2 * q + 1)];
   double Dn[4][2][2], Rt[4][2][2], dl[2], du[4][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) dl[i] = a.dL[gi0 + br + i];
@@ -614,11 +678,15 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
 #pragma unroll
       for (int i = 0; i < 2; ++i) pv[c][i] = double2{0.0, 0.0};
   }
+  // the factor blocks go to LDS with their 2 x 2 diagonal blocks zeroed: the
+  // block sweep takes the one off-diagonal entry of each (l10, u01) from a
+  // register, and the zeros make the lane's own block a zero-weight source
 #pragma unroll
   for (int s = 0; s < 16; ++s) {
     const int e = t + NT * s, r = e >> 6, x = e & 63;
-    sm.Ls[r][x] = lv[s];
-    sm.Us[r][x] = uv[s];
+    const bool dg = (r >> 1) == (x >> 1);
+    sm.Ls[r][x] = dg ? 0.0 : lv[s];
+    sm.Us[r][x] = dg ? 0.0 : uv[s];
   }
   if (t < TB) {
     *reinterpret_cast<double2*>(&sm.Ls[t][TB]) = double2{0.0, 0.0};
@@ -679,21 +747,38 @@ __device__ void run_sweep(const StageArgs& a, int I, int J, SweepSmem& sm) {
         for (int j = 0; j < 2; ++j) Rt[c][i][j] += sm.x.T[br + i][SS * c + 2 * q + j];
   }
   __syncthreads();
-  // the band's rows of Et / Ct start at zero: the block sweep reads a
-  // (zero-weighted) source block before it is written
+  // Et / Ct start at zero, their padding columns included: the block sweep
+  // reads (zero-weighted) source blocks before they are written, and its
+  // C-source reads of the first sub-tile reach back into the padding of the
+  // row before; every wave zeroes its band, and the barrier makes the whole
+  // arrays zero before any wave sweeps
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
     const int e = l + 64 * s, r = SS * w + (e >> 5), x = 2 * (e & 31);
     *reinterpret_cast<double2*>(&sm.x.t.Et[r][x]) = double2{0.0, 0.0};
     *reinterpret_cast<double2*>(&sm.x.t.Ct[r][x]) = double2{0.0, 0.0};
   }
+  if (l < 2 * SS) {
+    double(*arr)[TP] = l < SS ? sm.x.t.Et : sm.x.t.Ct;
+    *reinterpret_cast<double2*>(&arr[SS * w + (l & (SS - 1))][TB]) = double2{0.0, 0.0};
+  }
   Band bd;
   bd.w = w; bd.l = l; bd.p = p; bd.q = q; bd.br = br; bd.gi0 = gi0; bd.gj0 = gj0;
   bd.Et = a.E + tile_off(I, J, a.NT);
   bd.Ct = a.C + tile_off(I, J, a.NT);
-  bd.l10 = sm.Ls[br + 1][br];
+  bd.l10 = l10v;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) bd.u01[c] = u01v[c];
   bd.dl[0] = dl[0];
   bd.dl[1] = dl[1];
+  bd.interior = gi0 + TB <= a.m && gj0 + TB <= a.n;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    bd.zr[i] = a.Z + (int64_t)(gi0 + br + i) * a.ldz + (int64_t)(gj0 + 2 * q) * a.cstep;
+    bd.yr[i] = a.Y ? (void*)((T*)a.Y + (int64_t)(gi0 + br + i) * a.ldy + (int64_t)(gj0 + 2 * q) * a.cstep)
+                   : nullptr;
+  }
+  __syncthreads();
 
   double part = 0.0;
   int bad = 0;
