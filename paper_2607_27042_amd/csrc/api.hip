@@ -33,12 +33,13 @@ static void free_all(Factors* f) {
   f->allocations.clear();
   if (f->ev_near) (void)hipEventDestroy(f->ev_near);
   if (f->ev_far) (void)hipEventDestroy(f->ev_far);
+  if (f->ev_far1) (void)hipEventDestroy(f->ev_far1);
   for (hipEvent_t ev : f->stage_ev) (void)hipEventDestroy(ev);
   f->stage_ev.clear();
   if (f->aux) (void)hipStreamDestroy(f->aux);
   if (f->ev_own) (void)hipEventDestroy(f->ev_own);
   if (f->own) (void)hipStreamDestroy(f->own);
-  f->ev_near = f->ev_far = f->ev_own = nullptr;
+  f->ev_near = f->ev_far = f->ev_far1 = f->ev_own = nullptr;
   f->aux = f->own = nullptr;
   free_schedule(f->sched);
 }
@@ -149,6 +150,7 @@ gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
     he = hipStreamCreateWithFlags(&f->aux, hipStreamNonBlocking);
     if (he == hipSuccess) he = hipEventCreateWithFlags(&f->ev_near, hipEventDisableTiming);
     if (he == hipSuccess) he = hipEventCreateWithFlags(&f->ev_far, hipEventDisableTiming);
+    if (he == hipSuccess) he = hipEventCreateWithFlags(&f->ev_far1, hipEventDisableTiming);
     if (he != hipSuccess) st = hip_fail(he, "stream / event creation");
   }
   if (st == GPTQ2D_OK) {

@@ -878,10 +878,11 @@ __global__ __launch_bounds__(NT) void k_update(FacArgs f0, UpdRange r, BatchCtx 
 
 // ---------------------------------------------------------------------------
 // The far part of a group's trailing update on 128 x 128 tiles, for the
-// group of panels g0 .. g1-1 and the block rows / columns from g2 on (g0, g2
-// even):
-//   Q tiles (BI >= BJ >= g2/2):  Q -= Lc[BI][g0:g1] Lc[BJ][g0:g1]^T
-//   S tiles (BI >= g2/2, BJ < g0/2): S += Lc[BI][g0:g1] Li[g0:g1][BJ]
+// group of panels g0 .. g1-1 and the block columns of Q / block rows of S
+// g2 .. g3-1 (g0, g2 even; g3 even or at least the block count, which
+// means up to the end):
+//   Q tiles (BI >= BJ, g2/2 <= BJ < g3/2):  Q -= Lc[BI][g0:g1] Lc[BJ][g0:g1]^T
+//   S tiles (g2/2 <= BI < g3/2, BJ < g0/2): S += Lc[BI][g0:g1] Li[g0:g1][BJ]
 // with the same meaning as in k_update (the group's own S columns stay
 // there). Four waves, each a 64 x 64 quadrant as 4 x 4 MFMA blocks; the
 // accumulators start from the old values (the left operand enters negated
@@ -1007,20 +1008,38 @@ __device__ void upd_tile(double* out, int64_t ldo, const double* Ap, int64_t lda
   }
 }
 
-__device__ void update128_tile(const FacArgs& f, int g0, int g1, int g2, int b, UpdChunk* buf) {
+// Q tiles in the 128-wide block columns t0 <= BJ < t1 (every row BI >= BJ)
+// and S tiles in the block rows t0 <= BI < t1; t1 = nb2 is the whole
+// trailing triangle, enumerated row by row, a narrower range column by column.
+__host__ __device__ __forceinline__ int far_q_count(int nb2, int t0, int t1) {
+  return t1 >= nb2 ? (nb2 - t0) * (nb2 - t0 + 1) / 2 : (t1 - t0) * (2 * nb2 - t0 - t1 + 1) / 2;
+}
+
+__device__ void update128_tile(const FacArgs& f, int g0, int g1, int g2, int g3, int b, UpdChunk* buf) {
   for (int s = 0; s < 2; ++s) {
     const Side& sd = f.s[s];
     const int nb = sd.nb;
     if (g0 >= nb || g1 <= g0) continue;
-    const int nb2 = (nb + 1) / 2, t0 = g2 / 2;
-    if (t0 >= nb2) continue;
-    const int nq = (nb2 - t0) * (nb2 - t0 + 1) / 2, ns = (nb2 - t0) * (g0 / 2);
+    const int nb2 = (nb + 1) / 2, t0 = g2 / 2, t1 = g3 >= nb ? nb2 : g3 / 2;
+    if (t0 >= t1) continue;
+    const int nq = far_q_count(nb2, t0, t1), ns = (t1 - t0) * (g0 / 2);
     const int K = TB * (min(g1, nb) - g0);
     const int64_t dp = sd.dp;
     if (b < nq) {
-      int bi, bj;
-      tri_index(b, bi, bj);  // bi >= bj, relative to t0
-      const int BI = t0 + bi, BJ = t0 + bj;
+      int BI, BJ;
+      if (t1 >= nb2) {
+        int bi, bj;
+        tri_index(b, bi, bj);  // bi >= bj, relative to t0
+        BI = t0 + bi;
+        BJ = t0 + bj;
+      } else {
+        BJ = t0;
+        while (b >= nb2 - BJ) {
+          b -= nb2 - BJ;
+          ++BJ;
+        }
+        BI = BJ + b;
+      }
       upd_tile<1>(sd.gr + (int64_t)128 * BI * dp + 128 * BJ, dp,
                   sd.gr + (int64_t)128 * BI * dp + TB * g0, dp,
                   sd.gr + (int64_t)128 * BJ * dp + TB * g0, dp, K,
@@ -1044,13 +1063,14 @@ __device__ void update128_tile(const FacArgs& f, int g0, int g1, int g2, int b, 
 // smaller than the device leaves compute units to the diagonal blocks and
 // panels that run beside it on the other stream
 template <bool BAT>
-__global__ __launch_bounds__(NT) void k_update128(FacArgs f0, int g0, int g1, int g2, int ntile, BatchCtx bc) {
+__global__ __launch_bounds__(NT) void k_update128(FacArgs f0, int g0, int g1, int g2, int g3, int ntile,
+                                                  BatchCtx bc) {
   __shared__ UpdChunk buf[2];
   const FacArgs& f = BAT ? bat_prob<BAT>(bc)->base->f : f0;
   const int bid = bat_block<BAT>(bc), grid = bat_grid<BAT>(bc);
   for (int b = bid; b < ntile; b += grid) {
     if (b != bid) __syncthreads();  // the staging buffers are reused
-    update128_tile(f, g0, g1, g2, b, buf);
+    update128_tile(f, g0, g1, g2, g3, b, buf);
   }
 }
 
@@ -1213,13 +1233,13 @@ static int h_upd_count(int nb, const UpdRange& r) {
 }
 
 // work groups of k_update128 for one side (see there)
-static void h_far_counts(int nb, int g0, int g1, int g2, int& nq, int& ns) {
+static void h_far_counts(int nb, int g0, int g1, int g2, int g3, int& nq, int& ns) {
   nq = ns = 0;
   if (g0 >= nb || g1 <= g0) return;
-  const int nb2 = (nb + 1) / 2, t0 = g2 / 2;
-  if (t0 >= nb2) return;
-  nq = (nb2 - t0) * (nb2 - t0 + 1) / 2;
-  ns = (nb2 - t0) * (g0 / 2);
+  const int nb2 = (nb + 1) / 2, t0 = g2 / 2, t1 = g3 >= nb ? nb2 : g3 / 2;
+  if (t0 >= t1) return;
+  nq = far_q_count(nb2, t0, t1);
+  ns = (t1 - t0) * (g0 / 2);
 }
 
 // The factorisation of one problem (tab == nullptr: its inputs A, B), or of
@@ -1292,21 +1312,52 @@ static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq
       hipLaunchKernelGGL(HIP_KERNEL_NAME(k_update<BT>), g, dim3(NT), 0, q, a, r, bc);
     });
   };
+  // The far part of group g0 .. g1-1 for the block columns / rows ga .. gb-1,
+  // on the second stream: the bulk on 128 x 128 tiles, the inverse columns of
+  // the group itself (variable depth, first contribution overwrites) on 64 x 64.
+  auto far_update = [&](int g0, int g1, int ga, int gb) {
+    int fq0, fs0, fq1, fs1;
+    h_far_counts(nb0, g0, g1, ga, gb, fq0, fs0);
+    h_far_counts(nb1, g0, g1, ga, gb, fq1, fs1);
+    const int nfar = fq0 + fs0 + fq1 + fs1;
+    if (nfar > 0) {
+      int units = 256;
+      (void)hipDeviceGetAttribute(&units, hipDeviceAttributeMultiprocessorCount, f.device);
+      // a far update of a few tiles per compute unit leaves at least 32 units
+      // to the diagonal blocks, panels and near updates beside it (measured
+      // best at 4096), and spreads its tiles evenly over as few work groups as
+      // the same number of rounds needs, so that the rest of the device stays
+      // free; a larger one is the longer of the two streams and takes every
+      // unit (a batch fills the device by itself: one tile per work group)
+      int grid = nfar;
+      if (!tab && nfar <= 4 * units) {
+        const int rounds = (nfar + units - 33) / (units - 32);
+        grid = (nfar + rounds - 1) / rounds;
+      }
+      go(grid, f.aux, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+        constexpr bool BT = decltype(bat)::value;
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_update128<BT>), g, dim3(NT), 0, st, a, g0, g1, ga, gb, nfar, bc);
+      });
+    }
+    update(UpdRange{ga, ga, ga, gb, g0, g1, g0, -1}, f.aux);
+  };
   // Groups of GROUP panels (an even count: the far part works on pairs of
   // block columns). Inside a group, before each panel, its column of Q and
   // row of S receive the group's earlier panels (left-looking, so that the
   // critical chain has few work groups); afterwards the whole group updates
   // everything beyond it with (64 GROUP)-deep products: the next group's
   // columns on the caller's stream (they are needed first), the rest on the
-  // second stream, where it overlaps the next group's diagonal blocks and
-  // panels. Before touching tiles that the far part writes, the caller's
-  // stream waits for it. Eight panels per group from 96 block columns on
-  // (measured faster at 8192), four below (at 4096).
+  // second stream, where it overlaps the next group's panels. The second
+  // stream takes the group after next first and marks its end with an event:
+  // the next group's near update writes those columns and waits for that
+  // part only, not for the rest behind it. Eight panels per group from 96
+  // block columns on (measured faster at 8192), four below (at 4096).
   const int GROUP = nbmax > 96 ? 8 : 4;
   hipError_t he = hipSuccess;
-  bool far_pending = false;
+  bool far_pending = false, far1_pending = false;
   for (int g0 = 0; g0 < nbmax; g0 += GROUP) {
     const int g1 = std::min(g0 + GROUP, nbmax), g2 = std::min(g1 + GROUP, nbmax);
+    const int g3 = std::min(g2 + GROUP, nbmax);
     for (int kb = g0; kb < g1; ++kb) {
       // the diagonal block of every later panel is factored by the update
       // that completes it (the in-group update of the panel before, or the
@@ -1326,36 +1377,23 @@ static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq
       // columns wait for their own turn)
       if (kb + 1 < g1) update(UpdRange{kb + 1, kb + 2, kb + 1, kb + 2, g0, kb + 1, 0, kb + 1}, s);
     }
-    if (far_pending) {
-      he = hipStreamWaitEvent(s, f.ev_far, 0);
+    if (far1_pending) {
+      // the previous group's far update of the columns g1 .. g2-1 (and,
+      // earlier on the same stream, everything older that reaches them)
+      he = hipStreamWaitEvent(s, f.ev_far1, 0);
       if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
-      far_pending = false;
+      far1_pending = false;
     }
     update(UpdRange{g1, g2, g1, g2, g0, g1, 0, g1}, s);
     if (g2 < nbmax) {
       he = hipEventRecord(f.ev_near, s);
       if (he == hipSuccess) he = hipStreamWaitEvent(f.aux, f.ev_near, 0);
       if (he != hipSuccess) return hip_fail(he, "event record / wait");
-      // the bulk on 128 x 128 tiles; the inverse columns of the group
-      // itself (variable depth, first contribution overwrites) on 64 x 64
-      int fq0, fs0, fq1, fs1;
-      h_far_counts(nb0, g0, g1, g2, fq0, fs0);
-      h_far_counts(nb1, g0, g1, g2, fq1, fs1);
-      const int nfar = fq0 + fs0 + fq1 + fs1;
-      if (nfar > 0) {
-        int units = 256;
-        (void)hipDeviceGetAttribute(&units, hipDeviceAttributeMultiprocessorCount, f.device);
-        // a far update of a few tiles per compute unit leaves 32 units to the
-        // diagonal blocks and panels beside it (measured best at 4096); a
-        // larger one is the longer of the two streams and takes every unit
-        // (a batch fills the device by itself: one tile per work group)
-        const int grid = tab || nfar > 4 * units ? nfar : std::max(1, std::min(nfar, units - 32));
-        go(grid, f.aux, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
-          constexpr bool BT = decltype(bat)::value;
-          hipLaunchKernelGGL(HIP_KERNEL_NAME(k_update128<BT>), g, dim3(NT), 0, st, a, g0, g1, g2, nfar, bc);
-        });
-      }
-      update(UpdRange{g2, g2, g2, nbmax, g0, g1, g0, -1}, f.aux);
+      far_update(g0, g1, g2, g3);
+      he = hipEventRecord(f.ev_far1, f.aux);
+      if (he != hipSuccess) return hip_fail(he, "hipEventRecord");
+      far1_pending = true;
+      if (g3 < nbmax) far_update(g0, g1, g3, nbmax);
       he = hipEventRecord(f.ev_far, f.aux);
       if (he != hipSuccess) return hip_fail(he, "hipEventRecord");
       far_pending = true;

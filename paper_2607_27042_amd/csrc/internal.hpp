@@ -51,7 +51,7 @@ struct Factors {
   // second stream of the factorisation: the far part of each group's
   // trailing update runs there, next to the following group's panels
   hipStream_t aux = nullptr;
-  hipEvent_t ev_near = nullptr, ev_far = nullptr;
+  hipEvent_t ev_near = nullptr, ev_far = nullptr, ev_far1 = nullptr;
   // stream of this handle's factorisation inside a batched call (created on
   // first use) and the event that marks its end
   hipStream_t own = nullptr;
