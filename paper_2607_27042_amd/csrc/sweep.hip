@@ -485,23 +485,38 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
   const double* const pu0 = &sm.Us[0][0] + uc + 2 * q;
   const int lcol = SS * w - 2 - 2 * q;  // weight column of step k: lcol + 2 k
   const int urow = uc - 2 - 2 * p;      // weight row of step k: urow + 2 k
+  // the weights of step k do not depend on the sweep: they are read one step
+  // ahead, after that step's sources, so that the wait for the sources (the
+  // errors and C just written by the step before) covers four reads only
+  double2 wl[2][2], wu[2][2];
+  auto weights = [&](int k, double2(&l)[2], double2(&u)[2]) {
+    const bool vr = (unsigned)(k - 1 - q) < (unsigned)p;  // source block row k-1-q above
+    const bool vc = (unsigned)(k - 1 - p) < (unsigned)q;  // source block column k-1-p left
+    const double* pl = pl0 + (vr ? lcol + 2 * k : TB);
+    const double* pu = pu0 + (vc ? urow + 2 * k : TB) * TP;
+    l[0] = *reinterpret_cast<const double2*>(pl);
+    l[1] = *reinterpret_cast<const double2*>(pl + TP);
+    u[0] = *reinterpret_cast<const double2*>(pu);
+    u[1] = *reinterpret_cast<const double2*>(pu + TP);
+  };
+  weights(0, wl[0], wu[0]);
   double yf[2][2], cf[2][2], ef[2][2];
 #pragma unroll
   for (int k = 0; k < SS - 1; ++k) {
-    const bool vr = (unsigned)(k - 1 - q) < (unsigned)p;  // source block row k-1-q above
-    const bool vc = (unsigned)(k - 1 - p) < (unsigned)q;  // source block column k-1-p left
     const double* pe = pe0 + 2 * k * TP;
     const double* pc = pc0 + 2 * k;
-    const double* pl = pl0 + (vr ? lcol + 2 * k : TB);
-    const double* pu = pu0 + (vc ? urow + 2 * k : TB) * TP;
     const double2 e0 = *reinterpret_cast<const double2*>(pe);
     const double2 e1 = *reinterpret_cast<const double2*>(pe + TP);
-    const double2 l0 = *reinterpret_cast<const double2*>(pl);
-    const double2 l1 = *reinterpret_cast<const double2*>(pl + TP);
     const double2 c0 = *reinterpret_cast<const double2*>(pc);
     const double2 c1 = *reinterpret_cast<const double2*>(pc + TP);
-    const double2 v0 = *reinterpret_cast<const double2*>(pu);
-    const double2 v1 = *reinterpret_cast<const double2*>(pu + TP);
+    // (LDS serves a wave's requests in order: the weight reads go out right
+    // behind the source reads, so that they are done before this step's
+    // writes and the next step's source reads)
+    __builtin_amdgcn_sched_barrier(0);
+    if (k + 1 < SS - 1) weights(k + 1, wl[(k + 1) & 1], wu[(k + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);
+    const double2 l0 = wl[k & 1][0], l1 = wl[k & 1][1];
+    const double2 v0 = wu[k & 1][0], v1 = wu[k & 1][1];
     Dc[0][0] = fma(l0.y, e1.x, fma(l0.x, e0.x, Dc[0][0]));
     Dc[0][1] = fma(l0.y, e1.y, fma(l0.x, e0.y, Dc[0][1]));
     Dc[1][0] = fma(l1.y, e1.x, fma(l1.x, e0.x, Dc[1][0]));
