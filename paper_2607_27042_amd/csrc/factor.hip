@@ -901,17 +901,22 @@ struct UpdChunk {
   };
 };
 
-// (i0, i1 select the part i0 <= i < i1 of the loads)
+// Work groups of the far update: eight waves, two per SIMD, so that one
+// wave's MFMAs run while the other waits (load issue, barrier).
+constexpr int UT = 512;
+
+// Chunk c of both operands into d: the 32 four-row blocks of each, wave w
+// the blocks j = w + 8 i (i0 <= i < i1 of i < 4).
 template <int BT>
 __device__ __forceinline__ void upd_issue(const double* Ap, int64_t lda, const double* Bp, int64_t ldb,
                                           int c, int nr, int nc, UpdChunk& d, int w, int l, int i0 = 0,
-                                          int i1 = 8) {
+                                          int i1 = 4) {
   typedef __attribute__((address_space(3))) void lds_v;
   const int ar = l >> 4, ap = (l & 15) ^ ar;
   const int64_t k0 = (int64_t)c * GQ;
 #pragma unroll
   for (int i = i0; i < i1; ++i) {
-    const int j = w + 4 * i;
+    const int j = w + 8 * i;
     const double* pa = Ap + (int64_t)min(4 * j + ar, TB * nr - 1) * lda + k0 + 2 * ap;
     __builtin_amdgcn_global_load_lds((const void*)pa, (lds_v*)&d.a[j][0], 16, 0, 0);
     if (BT) {
@@ -924,21 +929,24 @@ __device__ __forceinline__ void upd_issue(const double* Ap, int64_t lda, const d
   }
 }
 
+// One 128 x 128 tile: wave w computes rows 64 qr .., columns 64 qc + 32 h ..
+// (qr = (w >> 1) & 1, qc = w & 1, h = w >> 2) as 4 x 2 MFMA blocks.
 template <int BT>
 __device__ void upd_tile(double* out, int64_t ldo, const double* Ap, int64_t lda, const double* Bp,
                          int64_t ldb, int K, int nr, int nc, bool diag, UpdChunk* buf) {
   const int t = threadIdx.x, w = t >> 6, l = t & 63;
-  const int qr = w >> 1, qc = w & 1, r0 = l & 15, rr = r0 & 3;
+  const int qr = (w >> 1) & 1, qc = w & 1, h = w >> 2, r0 = l & 15, rr = r0 & 3;
   const bool mine = qr < nr && qc < nc && !(diag && qr < qc);
   const double sgn = BT ? -1.0 : 1.0;
-  double* o = out + (int64_t)(64 * qr + (l >> 4)) * ldo + 64 * qc + (l & 15);
-  d4 acc[4][4];
+  const int cb = 64 * qc + 32 * h;
+  double* o = out + (int64_t)(64 * qr + (l >> 4)) * ldo + cb + (l & 15);
+  d4 acc[4][2];
   upd_issue<BT>(Ap, lda, Bp, ldb, 0, nr, nc, buf[0], w, l);
   if (mine) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[i][j][r] = o[(int64_t)(16 * i + 4 * r) * ldo + 16 * j];
     __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): no wait for them inside the loop
@@ -946,53 +954,53 @@ __device__ void upd_tile(double* out, int64_t ldo, const double* Ap, int64_t lda
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
+      for (int j = 0; j < 2; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
   }
   const int nch = K / GQ;
   for (int c = 0; c < nch; ++c) {
     // the next chunk's loads in two halves, the second half-way through this
-    // chunk's MFMAs (one batch stalls the wave's issue until the memory
-    // pipeline takes it)
+    // chunk's MFMAs
     const bool more = c + 1 < nch;
     if (more) {
-      upd_issue<BT>(Ap, lda, Bp, ldb, c + 1, nr, nc, buf[(c + 1) & 1], w, l, 0, 4);
-      __builtin_amdgcn_s_waitcnt(0x0f78);  // vmcnt(8): chunk c has landed
+      upd_issue<BT>(Ap, lda, Bp, ldb, c + 1, nr, nc, buf[(c + 1) & 1], w, l, 0, 2);
+      __builtin_amdgcn_s_waitcnt(0x0f74);  // vmcnt(4): chunk c has landed
     } else {
       __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     }
     asm volatile("s_barrier" ::: "memory");  // the wait above covers this wave's part
     const UpdChunk& st = buf[c & 1];
-    double av[2][4], bv[2][4];
+    double av[2][4], bv[2][2];
 #pragma unroll
     for (int kk = -1; kk < GQ / 4; ++kk) {
       const int nx = (kk + 1) & 1;
       if (kk == GQ / 8 && more) {
         __builtin_amdgcn_sched_barrier(0);
-        upd_issue<BT>(Ap, lda, Bp, ldb, c + 1, nr, nc, buf[(c + 1) & 1], w, l, 4, 8);
+        upd_issue<BT>(Ap, lda, Bp, ldb, c + 1, nr, nc, buf[(c + 1) & 1], w, l, 2, 4);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (kk + 1 < GQ / 4) {
         const int k = 4 * (kk + 1) + (l >> 4), kp = 2 * (kk + 1) + (l >> 5);
         const int ao = GQ * rr + 2 * (kp ^ rr) + ((l >> 4) & 1);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          av[nx][i] = sgn * st.a[(64 * qr + 16 * i + r0) >> 2][ao];
-          bv[nx][i] = BT ? st.bt[(64 * qc + 16 * i + r0) >> 2][ao] : st.b[k][64 * qc + 16 * i + r0];
-        }
+        for (int i = 0; i < 4; ++i) av[nx][i] = sgn * st.a[(64 * qr + 16 * i + r0) >> 2][ao];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          bv[nx][j] = BT ? st.bt[(cb + 16 * j + r0) >> 2][ao] : st.b[k][cb + 16 * j + r0];
       }
       if (kk >= 0) {
         const int cur = kk & 1;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
+          for (int j = 0; j < 2; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[cur][i], bv[cur][j], acc[i][j], 0, 0, 0);
         if (kk + 1 < GQ / 4) {
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          for (int u = 0; u < 6; ++u) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
           }
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         }
       }
     }
@@ -1002,7 +1010,7 @@ __device__ void upd_tile(double* out, int64_t ldo, const double* Ap, int64_t lda
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) o[(int64_t)(16 * i + 4 * r) * ldo + 16 * j] = acc[i][j][r];
   }
@@ -1063,13 +1071,18 @@ __device__ void update128_tile(const FacArgs& f, int g0, int g1, int g2, int g3,
 // smaller than the device leaves compute units to the diagonal blocks and
 // panels that run beside it on the other stream
 template <bool BAT>
-__global__ __launch_bounds__(NT) void k_update128(FacArgs f0, int g0, int g1, int g2, int g3, int ntile,
+__global__ __launch_bounds__(UT) void k_update128(FacArgs f0, int g0, int g1, int g2, int g3, int ntile,
                                                   BatchCtx bc) {
   __shared__ UpdChunk buf[2];
   const FacArgs& f = BAT ? bat_prob<BAT>(bc)->base->f : f0;
   const int bid = bat_block<BAT>(bc), grid = bat_grid<BAT>(bc);
-  for (int b = bid; b < ntile; b += grid) {
-    if (b != bid) __syncthreads();  // the staging buffers are reused
+  // work groups are dealt round-robin to the eight L2 domains: each domain
+  // takes a contiguous run of every round's tiles, so that the tiles it runs
+  // at the same time share their row panel (rows are enumerated tile by tile)
+  const int q8 = grid / 8, r8 = grid % 8, x = bid % 8;
+  const int pos = x * q8 + min(x, r8) + bid / 8;
+  for (int b = pos; b < ntile; b += grid) {
+    if (b != pos) __syncthreads();  // the staging buffers are reused
     update128_tile(f, g0, g1, g2, g3, b, buf);
   }
 }
@@ -1312,10 +1325,11 @@ static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq
       hipLaunchKernelGGL(HIP_KERNEL_NAME(k_update<BT>), g, dim3(NT), 0, q, a, r, bc);
     });
   };
-  // The far part of group g0 .. g1-1 for the block columns / rows ga .. gb-1,
-  // on the second stream: the bulk on 128 x 128 tiles, the inverse columns of
-  // the group itself (variable depth, first contribution overwrites) on 64 x 64.
-  auto far_update = [&](int g0, int g1, int ga, int gb) {
+  // The trailing update with group g0 .. g1-1 of the block columns / rows
+  // ga .. gb-1 on stream st: the bulk on 128 x 128 tiles, the inverse columns
+  // of the group itself (variable depth, first contribution overwrites) on
+  // 64 x 64.
+  auto group_update = [&](int g0, int g1, int ga, int gb, hipStream_t st0) {
     int fq0, fs0, fq1, fs1;
     h_far_counts(nb0, g0, g1, ga, gb, fq0, fs0);
     h_far_counts(nb1, g0, g1, ga, gb, fq1, fs1);
@@ -1334,12 +1348,12 @@ static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq
         const int rounds = (nfar + units - 33) / (units - 32);
         grid = (nfar + rounds - 1) / rounds;
       }
-      go(grid, f.aux, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+      go(grid, st0, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
         constexpr bool BT = decltype(bat)::value;
-        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_update128<BT>), g, dim3(NT), 0, st, a, g0, g1, ga, gb, nfar, bc);
+        hipLaunchKernelGGL(HIP_KERNEL_NAME(k_update128<BT>), g, dim3(UT), 0, st, a, g0, g1, ga, gb, nfar, bc);
       });
     }
-    update(UpdRange{ga, ga, ga, gb, g0, g1, g0, -1}, f.aux);
+    update(UpdRange{ga, ga, ga, gb, g0, g1, g0, -1}, st0);
   };
   // Groups of GROUP panels (an even count: the far part works on pairs of
   // block columns). Inside a group, before each panel, its column of Q and
@@ -1384,16 +1398,19 @@ static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq
       if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
       far1_pending = false;
     }
+    // the next group's columns (the near update, on this stream: they are
+    // needed first; 64 x 64 tiles, the first diagonal block factored by the
+    // work group that completes it)
     update(UpdRange{g1, g2, g1, g2, g0, g1, 0, g1}, s);
     if (g2 < nbmax) {
       he = hipEventRecord(f.ev_near, s);
       if (he == hipSuccess) he = hipStreamWaitEvent(f.aux, f.ev_near, 0);
       if (he != hipSuccess) return hip_fail(he, "event record / wait");
-      far_update(g0, g1, g2, g3);
+      group_update(g0, g1, g2, g3, f.aux);
       he = hipEventRecord(f.ev_far1, f.aux);
       if (he != hipSuccess) return hip_fail(he, "hipEventRecord");
       far1_pending = true;
-      if (g3 < nbmax) far_update(g0, g1, g3, nbmax);
+      if (g3 < nbmax) group_update(g0, g1, g3, nbmax, f.aux);
       he = hipEventRecord(f.ev_far, f.aux);
       if (he != hipSuccess) return hip_fail(he, "hipEventRecord");
       far_pending = true;
