@@ -481,10 +481,16 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
   // a constant offset: no address arithmetic in the steps)
   const double* const pe0 = &sm.x.t.Et[0][0] + (SS * w - 2 - 2 * q) * TP + uc + 2 * q;
   const double* const pc0 = &sm.x.t.Ct[0][0] + br * TP + uc - 2 - 2 * p;
-  const double* const pl0 = &sm.Ls[br][0];
-  const double* const pu0 = &sm.Us[0][0] + uc + 2 * q;
-  const int lcol = SS * w - 2 - 2 * q;  // weight column of step k: lcol + 2 k
-  const int urow = uc - 2 - 2 * p;      // weight row of step k: urow + 2 k
+  // weights of step k: L rows br, br+1 at columns SS w - 2 - 2 q + 2 k, and U
+  // rows uc - 2 - 2 p + 2 k, +1 at columns uc + 2q, +1; a source that does not
+  // feed the lane reads zeros at the same step offset instead: the zero rows
+  // 64, 65 of Us for L (the offset runs along columns) and the zero columns
+  // 64, 65 of Ls for U (it runs along rows). So a step selects one of two
+  // bases per operand and adds a constant.
+  const double* const plv = &sm.Ls[br][0] + SS * w - 2 - 2 * q;
+  const double* const plz = &sm.Us[TB][0];
+  const double* const puv = &sm.Us[0][0] + (uc - 2 - 2 * p) * TP + uc + 2 * q;
+  const double* const puz = &sm.Ls[0][TB];
   // the weights of step k do not depend on the sweep: they are read one step
   // ahead, after that step's sources, so that the wait for the sources (the
   // errors and C just written by the step before) covers four reads only
@@ -492,8 +498,8 @@ __device__ __forceinline__ void sub_tile(const StageArgs& a, SweepSmem& sm, cons
   auto weights = [&](int k, double2(&l)[2], double2(&u)[2]) {
     const bool vr = (unsigned)(k - 1 - q) < (unsigned)p;  // source block row k-1-q above
     const bool vc = (unsigned)(k - 1 - p) < (unsigned)q;  // source block column k-1-p left
-    const double* pl = pl0 + (vr ? lcol + 2 * k : TB);
-    const double* pu = pu0 + (vc ? urow + 2 * k : TB) * TP;
+    const double* pl = (vr ? plv : plz) + 2 * k;
+    const double* pu = (vc ? puv : puz) + 2 * k * TP;
     l[0] = *reinterpret_cast<const double2*>(pl);
     l[1] = *reinterpret_cast<const double2*>(pl + TP);
     u[0] = *reinterpret_cast<const double2*>(pu);
