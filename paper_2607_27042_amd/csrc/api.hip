@@ -134,6 +134,11 @@ gptq2d_status gptq2d_factors_create(int m, int n, gptq2d_factors_t* out) {
     f->cus = 256;
   const size_t gpd = gram_part_doubles(f->m, f->n, f->cus);
   if (gpd > 0) A(&f->gpart, gpd);
+  const size_t gev = gram_env_ints(f->m, f->n);
+  if (gev > 0 && st == GPTQ2D_OK) {
+    st = alloc(f, &p, gev * sizeof(int));
+    if (st == GPTQ2D_OK) f->genv = (int*)p;
+  }
   if (st == GPTQ2D_OK) {
     st = alloc(f, &p, 256);
     if (st == GPTQ2D_OK) {

@@ -41,7 +41,8 @@ struct Side {
 struct FacArgs {
   Side s[2];
   int* flags;
-  int rev;  // reverse order: the index-reversed problem (A P, P B), so no reversal below
+  int* genv;  // Gram envelopes and work plan (GramView)
+  int rev;    // reverse order: the index-reversed problem (A P, P B), so no reversal below
 };
 
 // Batched factorisation: problems of one shape in common launches. Problem p
@@ -216,6 +217,17 @@ __global__ __launch_bounds__(NT) void k_gram(FacArgs f0, const T* A0, int64_t ld
 // The panel lives in the side's inverse buffer, which the factorisation fills
 // only later.
 //
+// While it writes the panel, k_gram_prep also records each 128-row block's
+// envelope: the range of 64-column blocks holding a nonzero entry. Entry
+// (p, q) of the Gram only gathers products S[p][k] S[q][k] with k in both
+// rows' envelopes; every other term is an exact zero, and adding it leaves a
+// floating-point sum unchanged, so the contraction of tile (bp, bq) runs over
+// the intersection of the two row blocks' envelopes and gives the same Gram.
+// A triangular basis (the Cholesky factor of a Gram, as in every workload
+// here) leaves about a third of the dense contraction; a dense one all of it.
+// k_gram_plan turns the envelopes into each tile's range of 32-deep chunks
+// and the division of all of them between the work groups (below).
+//
 // k_gram128 then forms Gr[p][q] = sum_k S[p][k] S[q][k] on the lower
 // 128 x 128 tiles: four waves, each a 64 x 64 quadrant as 4 x 4 MFMA blocks
 // (the upper quadrant of a diagonal tile is computed but not stored), the
@@ -224,6 +236,72 @@ __global__ __launch_bounds__(NT) void k_gram(FacArgs f0, const T* A0, int64_t ld
 // blocks of four, 16-byte pieces XOR-permuted by the row's position in the
 // block, 64 bytes of padding per block).
 // ---------------------------------------------------------------------------
+
+// The chunks of all 128 x 128 Gram tiles, tile by tile (side 0's tiles
+// first), form one sequence of work units, dealt out as G contiguous ranges
+// of nearly equal length, one per work group, so that no round of work groups
+// runs with most of the device idle. A range is at least as long as the
+// longest tile: a tile is either inside one range (stored directly) or split
+// between two neighbouring ranges, whose partial products go to a pair of
+// scratch slots (one per range boundary) and are added by k_gram_fix in a
+// fixed order. A tile's chunks are those its envelope leaves (an empty
+// intersection counts as one unit that stores zeros), so the division is
+// made on the device by k_gram_plan; the host fixes the launch grid from the
+// dense count, an upper bound for G.
+struct GramPlan {
+  int t0, t1;          // tiles of side 0 and side 1 on this path
+  int n0, n1;          // 128-row blocks of side 0 and side 1 on this path
+  int nch0, nch1;      // dense chunks per tile on each side
+  int64_t units;       // dense units: t0 nch0 + t1 nch1
+  int G;               // launch grid (work groups, an upper bound for the ranges)
+};
+
+// The envelope and plan buffer of a handle (ints): the total of units (an
+// int64) and the number of ranges, the envelope of every 128-row block of
+// each side (first and one past the last 64-column block with a nonzero
+// entry), each tile's first and one past its last chunk, and the prefix sum
+// of the tiles' unit counts (int64).
+struct GramView {
+  long long* U;
+  int* Geff;
+  int* emin[2];
+  int* emax[2];
+  int* clo;
+  int* chi;
+  long long* pre;
+};
+__host__ __device__ inline size_t gram_view_ints(int n0, int n1, int T) {
+  const size_t head = 4 + 2 * (size_t)n0 + 2 * (size_t)n1 + 2 * (size_t)T;
+  return (head + 1) / 2 * 2 + 2 * ((size_t)T + 1);
+}
+__host__ __device__ inline GramView gram_view(int* base, int n0, int n1, int T) {
+  GramView v;
+  v.U = (long long*)base;
+  v.Geff = base + 2;
+  v.emin[0] = base + 4;
+  v.emax[0] = v.emin[0] + n0;
+  v.emin[1] = v.emax[0] + n0;
+  v.emax[1] = v.emin[1] + n1;
+  v.clo = v.emax[1] + n1;
+  v.chi = v.clo + T;
+  const size_t head = 4 + 2 * (size_t)n0 + 2 * (size_t)n1 + 2 * (size_t)T;
+  v.pre = (long long*)(base + (head + 1) / 2 * 2);
+  return v;
+}
+__device__ __forceinline__ GramView gram_view(int* base, const GramPlan& pl) {
+  return gram_view(base, pl.n0, pl.n1, pl.t0 + pl.t1);
+}
+
+// Unit u (0 <= u < U) -> its tile: the last t with pre[t] <= u.
+__device__ __forceinline__ int gram_tile_of(const long long* pre, int T, long long u) {
+  int lo = 0, hi = T - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (pre[mid] <= u) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
 
 constexpr int GQ = 32;           // chunk depth
 constexpr int GA = 4 * GQ + 8;   // doubles per 4-row block
@@ -234,7 +312,7 @@ struct GramChunk {
 
 template <typename T, bool BAT>
 __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f0, const T* A0, int64_t lda0, const T* B0,
-                                                  int64_t ldb0, int sides, BatchCtx bc) {
+                                                  int64_t ldb0, int sides, GramPlan pl, BatchCtx bc) {
   __shared__ double tile[TB][TB + 1];
   const FacProb* pb = bat_prob<BAT>(bc);
   const FacArgs& f = BAT ? pb->base->f : f0;
@@ -251,6 +329,7 @@ __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f0, const T* A0, int64
   double* S = sd.li;
   const int t = threadIdx.x;
   const int rev = BAT ? (int)pb->rev : f0.rev;
+  bool nz = false;  // a nonzero entry in this thread's part of the block
   if (side == 0) {
     // A rows k0 + r, columns d-1-(i0+63) .. d-1-i0 (ascending; in reverse
     // order i0 .. i0+63), coalesced
@@ -258,7 +337,9 @@ __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f0, const T* A0, int64
 #pragma unroll
     for (int u = 0; u < 16; ++u) {
       const int e = t + NT * u, r = e >> 6, c = e & 63;  // c: column offset in A
-      tile[r][c] = (double)A[(int64_t)(k0 + r) * lda + c0 + c];
+      const double x = (double)A[(int64_t)(k0 + r) * lda + c0 + c];
+      tile[r][c] = x;
+      nz |= x != 0.0;
     }
     __syncthreads();
     // S[i0 + i][k0 + k] = A[k0 + k][d-1-(i0+i)] = tile[k][63 - i] (reverse order: tile[k][i])
@@ -272,8 +353,17 @@ __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f0, const T* A0, int64
     for (int u = 0; u < 16; ++u) {
       const int e = t + NT * u, i = e >> 6, k = e & 63;
       const int row = rev ? i0 + i : d - 1 - (i0 + i);
-      S[(int64_t)(i0 + i) * d + k0 + k] = (double)B[(int64_t)row * ldb + k0 + k];
+      const double x = (double)B[(int64_t)row * ldb + k0 + k];
+      S[(int64_t)(i0 + i) * d + k0 + k] = x;
+      nz |= x != 0.0;
     }
+  }
+  // the block's 64 columns join the envelope of its 128-row block (a NaN
+  // counts as nonzero; integer min and max do not depend on the order)
+  if (__syncthreads_or(nz) && threadIdx.x == 0) {
+    const GramView v = gram_view(f.genv, pl);
+    atomicMin(&v.emin[side][i0 >> 7], k0 >> 6);
+    atomicMax(&v.emax[side][i0 >> 7], (k0 >> 6) + 1);
   }
 }
 
@@ -292,27 +382,72 @@ __device__ __forceinline__ void gram_issue(const double* Sp, const double* Sq, i
   }
 }
 
-// The 32-deep chunks of all 128 x 128 Gram tiles, tile by tile (side 0's
-// tiles first), form one sequence of work units, dealt out as G contiguous
-// ranges of nearly equal length, one per work group, so that no round of
-// work groups runs with most of the device idle. A range is at least one
-// tile long: a tile is either inside one range (stored directly) or split
-// between two neighbouring ranges, whose partial products go to a pair of
-// scratch slots (one per range boundary) and are added by k_gram_fix in a
-// fixed order.
-struct GramPlan {
-  int t0, t1;          // tiles of side 0 and side 1 on this path
-  int nch0, nch1;      // chunks per tile on each side
-  int64_t units;       // t0 nch0 + t1 nch1
-  int G;               // work groups (ranges)
-  __host__ __device__ int64_t lo(int j) const { return units * j / G; }
-  // unit u -> side, tile, first chunk
-  __host__ __device__ void at(int64_t u, int& side, int& b, int& c) const {
-    const int64_t u0 = (int64_t)t0 * nch0;
-    if (u < u0) { side = 0; b = (int)(u / nch0); c = (int)(u % nch0); }
-    else { side = 1; b = (int)((u - u0) / nch1); c = (int)((u - u0) % nch1); }
+// The envelopes start empty (first past last).
+template <bool BAT>
+__global__ __launch_bounds__(NT) void k_gram_env_init(FacArgs f0, GramPlan pl, BatchCtx bc) {
+  const FacProb* pb = bat_prob<BAT>(bc);
+  const FacArgs& f = BAT ? pb->base->f : f0;
+  const GramView v = gram_view(f.genv, pl);
+  for (int i = threadIdx.x; i < pl.n0; i += NT) {
+    v.emin[0][i] = 0x7fffffff;
+    v.emax[0][i] = 0;
   }
-};
+  for (int i = threadIdx.x; i < pl.n1; i += NT) {
+    v.emin[1][i] = 0x7fffffff;
+    v.emax[1][i] = 0;
+  }
+}
+
+// Every tile's chunk range from the envelopes of its two row blocks, the
+// prefix sum of the unit counts, and the number of ranges: the launch grid,
+// or fewer so that a range is at least as long as the longest tile.
+constexpr int PLT = 1024;
+template <bool BAT>
+__global__ __launch_bounds__(PLT) void k_gram_plan(FacArgs f0, GramPlan pl, BatchCtx bc) {
+  __shared__ long long part[PLT];
+  __shared__ int mx[PLT];
+  const FacProb* pb = bat_prob<BAT>(bc);
+  const FacArgs& f = BAT ? pb->base->f : f0;
+  const GramView v = gram_view(f.genv, pl);
+  const int T = pl.t0 + pl.t1, t = threadIdx.x;
+  const int per = (T + PLT - 1) / PLT, a0 = min(T, t * per), a1 = min(T, a0 + per);
+  long long sum = 0;
+  int most = 0;
+  for (int i = a0; i < a1; ++i) {
+    const int side = i < pl.t0 ? 0 : 1;
+    int bp, bq;
+    tri_index(side ? i - pl.t0 : i, bp, bq);
+    const int lo = max(v.emin[side][bp], v.emin[side][bq]), hi = min(v.emax[side][bp], v.emax[side][bq]);
+    const bool empty = hi <= lo;
+    v.clo[i] = empty ? 0 : 2 * lo;  // an envelope block is two 32-deep chunks
+    v.chi[i] = empty ? 0 : 2 * hi;
+    const int cnt = empty ? 1 : 2 * (hi - lo);
+    sum += cnt;
+    most = max(most, cnt);
+  }
+  part[t] = sum;
+  mx[t] = most;
+  __syncthreads();
+  if (t == 0) {
+    long long run = 0;
+    int m = 1;
+    for (int i = 0; i < PLT; ++i) {
+      const long long x = part[i];
+      part[i] = run;
+      run += x;
+      m = max(m, mx[i]);
+    }
+    *v.U = run;
+    *v.Geff = (int)max(1LL, min((long long)pl.G, run / m));
+    v.pre[T] = run;
+  }
+  __syncthreads();
+  long long run = part[t];
+  for (int i = a0; i < a1; ++i) {
+    v.pre[i] = run;
+    run += v.chi[i] > v.clo[i] ? v.chi[i] - v.clo[i] : 1;
+  }
+}
 
 // Chunks c0 .. c1-1 of the tile (bp, bq) of one side into acc (zeroed here).
 __device__ __forceinline__ void gram_part(const Side& sd, int bp, int bq, int c0, int c1, GramChunk* buf,
@@ -326,7 +461,7 @@ __device__ __forceinline__ void gram_part(const Side& sd, int bp, int bq, int c0
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = d4{0.0, 0.0, 0.0, 0.0};
-  gram_issue(Sp, Sq, d, c0, buf[0], w, l);
+  if (c0 < c1) gram_issue(Sp, Sq, d, c0, buf[0], w, l);
   for (int c = c0; c < c1; ++c) {
     const int cb = (c - c0) & 1;
     // the next chunk's loads in two halves, the second half-way through this
@@ -408,32 +543,39 @@ __global__ __launch_bounds__(NT) void k_gram128(FacArgs f0, GramPlan pl, double*
   const FacProb* pb = bat_prob<BAT>(bc);
   const FacArgs& f = BAT ? pb->base->f : f0;
   double* part = BAT ? pb->base->gpart : part0;
+  const GramView v = gram_view(f.genv, pl);
   const int bid = bat_block<BAT>(bc);
+  const int G = *v.Geff, T = pl.t0 + pl.t1;
+  const long long U = *v.U;
   // work groups are dealt round-robin to the eight L2 domains (XCDs): give
   // each domain a contiguous run of ranges, so that the tiles it runs at the
   // same time share their row panel (tri_index enumerates row by row)
-  // (domain x holds the work groups i = x mod 8, q of them, and gets the
-  // ranges from x q + min(x, r) on, with q, r the quotient and remainder by 8)
-  const int q8 = pl.G / 8, r8 = pl.G % 8;
-  const int x = bid % 8;
-  const int jr = x * q8 + min(x, r8) + bid / 8;
-  const int64_t hi = pl.lo(jr + 1);
+  // (domain x holds the work groups i = x mod 8 and gets q ranges, plus one
+  // when x < r, from x q + min(x, r) on, with q, r the quotient and remainder
+  // of G by 8; the launch's further work groups have none)
+  const int q8 = G / 8, r8 = G % 8;
+  const int x = bid % 8, y = bid / 8;
+  if (y >= q8 + (x < r8 ? 1 : 0)) return;
+  const int jr = x * q8 + min(x, r8) + y;
+  const long long lo = U * jr / G, hi = U * (jr + 1) / G;
   d4 acc[4][4];
-  for (int64_t u = pl.lo(jr); u < hi;) {
-    int side, b, c0;
-    pl.at(u, side, b, c0);
+  int tile = lo < hi ? gram_tile_of(v.pre, T, lo) : 0;
+  for (long long u = lo; u < hi; ++tile) {
+    const int side = tile < pl.t0 ? 0 : 1;
     const Side& sd = f.s[side];
-    const int nch = side == 0 ? pl.nch0 : pl.nch1;
-    const int c1 = (int)min((int64_t)nch, c0 + (hi - u));
+    const long long p0 = v.pre[tile], p1 = v.pre[tile + 1];
+    const int clo = v.clo[tile], nreal = v.chi[tile] - clo;
+    const int o0 = (int)(u - p0), o1 = (int)(min(p1, hi) - p0);  // this range's units of the tile
+    const int c0 = clo + min(o0, nreal), c1 = clo + min(o1, nreal);
     int bp, bq;
-    tri_index(b, bp, bq);
-    if (u != pl.lo(jr)) __syncthreads();  // the staging buffers are reused
+    tri_index(side ? tile - pl.t0 : tile, bp, bq);
+    if (u != lo) __syncthreads();  // the staging buffers are reused
     gram_part(sd, bp, bq, c0, c1, buf, acc);
-    if (c0 == 0 && c1 == nch) {
+    if (u == p0 && min(p1, hi) == p1) {
       gram_store(sd, bp, bq, acc);
     } else {
       // the head of a tile ends this range (slot jr), the tail of one starts it (slot jr - 1)
-      double* o = c0 == 0 ? gram_slot(part, jr, 0) : gram_slot(part, jr - 1, 1);
+      double* o = u == p0 ? gram_slot(part, jr, 0) : gram_slot(part, jr - 1, 1);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -441,7 +583,7 @@ __global__ __launch_bounds__(NT) void k_gram128(FacArgs f0, GramPlan pl, double*
 #pragma unroll
           for (int r = 0; r < 4; ++r) o[(int64_t)(((i * 4 + j) * 4 + r) * NT)] = acc[i][j][r];
     }
-    u += c1 - c0;
+    u = min(p1, hi);
   }
 }
 
@@ -451,11 +593,13 @@ __global__ __launch_bounds__(NT) void k_gram_fix(FacArgs f0, GramPlan pl, const 
   const FacProb* pb = bat_prob<BAT>(bc);
   const FacArgs& f = BAT ? pb->base->f : f0;
   const double* part = BAT ? pb->base->gpart : part0;
+  const GramView v = gram_view(f.genv, pl);
   const int jr = bat_block<BAT>(bc);
-  const int64_t u = pl.lo(jr + 1);
-  int side, b, c;
-  pl.at(u, side, b, c);
-  if (c == 0) return;  // the boundary falls between tiles
+  const int G = *v.Geff, T = pl.t0 + pl.t1;
+  if (jr + 1 >= G) return;
+  const long long u = *v.U * (jr + 1) / G;
+  const int tile = gram_tile_of(v.pre, T, u);
+  if (u == v.pre[tile]) return;  // the boundary falls between tiles
   const double* h0 = gram_slot(const_cast<double*>(part), jr, 0);
   const double* h1 = gram_slot(const_cast<double*>(part), jr, 1);
   d4 acc[4][4];
@@ -468,30 +612,42 @@ __global__ __launch_bounds__(NT) void k_gram_fix(FacArgs f0, GramPlan pl, const 
         const int64_t e = (int64_t)(((i * 4 + j) * 4 + r) * NT);
         acc[i][j][r] = h0[e] + h1[e];
       }
+  const int side = tile < pl.t0 ? 0 : 1;
   int bp, bq;
-  tri_index(b, bp, bq);
+  tri_index(side ? tile - pl.t0 : tile, bp, bq);
   gram_store(f.s[side], bp, bq, acc);
 }
 
 static GramPlan gram_plan(int m, int n, int fast, int cus) {
   GramPlan pl;
   const int n0 = m / 128, n1 = n / 128;
-  pl.t0 = (fast & 1) ? n0 * (n0 + 1) / 2 : 0;
-  pl.t1 = (fast & 2) ? n1 * (n1 + 1) / 2 : 0;
+  pl.n0 = (fast & 1) ? n0 : 0;
+  pl.n1 = (fast & 2) ? n1 : 0;
+  pl.t0 = pl.n0 * (pl.n0 + 1) / 2;
+  pl.t1 = pl.n1 * (pl.n1 + 1) / 2;
   pl.nch0 = std::max(1, m / GQ);
   pl.nch1 = std::max(1, n / GQ);
   pl.units = (int64_t)pl.t0 * pl.nch0 + (int64_t)pl.t1 * pl.nch1;
   const int64_t nmax = std::max(pl.t0 ? pl.nch0 : 1, pl.t1 ? pl.nch1 : 1);
-  // every range at least one tile long: a tile meets at most one boundary
+  // every range at least one dense tile long: a tile meets at most one boundary
   pl.G = (int)std::max<int64_t>(1, std::min<int64_t>(std::max(cus, 1), pl.units / nmax));
   return pl;
 }
 
+static int fast_sides(int m, int n) { return (m % 128 == 0 ? 1 : 0) | (n % 128 == 0 ? 2 : 0); }
+
 size_t gram_part_doubles(int m, int n, int cus) {
-  const int fast = (m % 128 == 0 ? 1 : 0) | (n % 128 == 0 ? 2 : 0);
+  const int fast = fast_sides(m, n);
   if (!fast) return 0;
   const GramPlan pl = gram_plan(m, n, fast, cus);
   return pl.G > 1 ? (size_t)2 * pl.G * 16384 : 0;
+}
+
+size_t gram_env_ints(int m, int n) {
+  const int fast = fast_sides(m, n);
+  if (!fast) return 0;
+  const GramPlan pl = gram_plan(m, n, fast, 1);
+  return gram_view_ints(pl.n0, pl.n1, pl.t0 + pl.t1);
 }
 
 // ---------------------------------------------------------------------------
@@ -1233,6 +1389,7 @@ static FacArgs fac_args(Factors& f) {
     sd.nb = sd.dp / TB;
   }
   a.flags = f.flags;
+  a.genv = f.genv;
   a.rev = f.rev;
   return a;
 }
@@ -1288,16 +1445,24 @@ static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq
     }
   }
   if (fast) {
+    const GramPlan pl = gram_plan(f.m, f.n, fast, f.cus);
+    go(1, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+      constexpr bool BT = decltype(bat)::value;
+      hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram_env_init<BT>), g, dim3(NT), 0, st, a, pl, bc);
+    });
     go(nprep, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
       constexpr bool BT = decltype(bat)::value;
       if (dt == GPTQ2D_F32)
         hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram_prep<float, BT>), g, dim3(NT), 0, st, a,
-                           (const float*)A, lda, (const float*)B, ldb, fast, bc);
+                           (const float*)A, lda, (const float*)B, ldb, fast, pl, bc);
       else
         hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram_prep<double, BT>), g, dim3(NT), 0, st, a,
-                           (const double*)A, lda, (const double*)B, ldb, fast, bc);
+                           (const double*)A, lda, (const double*)B, ldb, fast, pl, bc);
     });
-    const GramPlan pl = gram_plan(f.m, f.n, fast, f.cus);
+    go(1, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
+      constexpr bool BT = decltype(bat)::value;
+      hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram_plan<BT>), g, dim3(PLT), 0, st, a, pl, bc);
+    });
     go(pl.G, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
       constexpr bool BT = decltype(bat)::value;
       hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram128<BT>), g, dim3(NT), 0, st, a, pl, f.gpart, bc);

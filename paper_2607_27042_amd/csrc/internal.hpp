@@ -47,6 +47,7 @@ struct Factors {
   double* dinv[2] = {nullptr, nullptr};  // inverses of its 64 x 64 diagonal blocks
   int* flags = nullptr;                  // device error bits of the factorisation
   double* gpart = nullptr;               // partial Gram tiles split between work groups
+  int* genv = nullptr;                   // Gram envelopes and the Gram work plan built from them
   int cus = 256;                         // compute units of the device
   // second stream of the factorisation: the far part of each group's
   // trailing update runs there, next to the following group's panels
@@ -116,6 +117,7 @@ gptq2d_status check_round_args(const Factors* f, gptq2d_dtype dt, const void* X,
 // factorisation launches (enqueued on stream, no synchronisation)
 // doubles of scratch for the Gram tiles split between work groups
 size_t gram_part_doubles(int m, int n, int cus);
+size_t gram_env_ints(int m, int n);
 // stream-ordered upload of host words into device memory (bytes and dst
 // multiples of 8; the host buffer may be reused on return)
 gptq2d_status enqueue_upload(void* dst, const void* src, size_t bytes, hipStream_t s);
