@@ -257,35 +257,34 @@ struct GramPlan {
 };
 
 // The envelope and plan buffer of a handle (ints): the total of units (an
-// int64) and the number of ranges, the envelope of every 128-row block of
-// each side (first and one past the last 64-column block with a nonzero
-// entry), each tile's first and one past its last chunk, and the prefix sum
-// of the tiles' unit counts (int64).
+// int64) and the number of ranges, each tile's first and one past its last
+// chunk, the prefix sum of the tiles' unit counts (int64), and per side the
+// nonzero votes of the panel's 64 x 64 blocks (one int per wave of the prep
+// kernel's work group: (d/64)^2 x 4).
 struct GramView {
   long long* U;
   int* Geff;
-  int* emin[2];
-  int* emax[2];
   int* clo;
   int* chi;
   long long* pre;
+  int* mask[2];
 };
+// (offsets in ints from a 256-byte aligned base: pre on 8 bytes, the votes
+// on 16 bytes, read as int4)
+__host__ __device__ inline size_t gram_pre_at(int T) { return (4 + 2 * (size_t)T + 1) / 2 * 2; }
+__host__ __device__ inline size_t gram_mask_at(int T) { return (gram_pre_at(T) + 2 * ((size_t)T + 1) + 3) / 4 * 4; }
 __host__ __device__ inline size_t gram_view_ints(int n0, int n1, int T) {
-  const size_t head = 4 + 2 * (size_t)n0 + 2 * (size_t)n1 + 2 * (size_t)T;
-  return (head + 1) / 2 * 2 + 2 * ((size_t)T + 1);
+  return gram_mask_at(T) + 16 * (size_t)n0 * n0 + 16 * (size_t)n1 * n1;
 }
 __host__ __device__ inline GramView gram_view(int* base, int n0, int n1, int T) {
   GramView v;
   v.U = (long long*)base;
   v.Geff = base + 2;
-  v.emin[0] = base + 4;
-  v.emax[0] = v.emin[0] + n0;
-  v.emin[1] = v.emax[0] + n0;
-  v.emax[1] = v.emin[1] + n1;
-  v.clo = v.emax[1] + n1;
+  v.clo = base + 4;
   v.chi = v.clo + T;
-  const size_t head = 4 + 2 * (size_t)n0 + 2 * (size_t)n1 + 2 * (size_t)T;
-  v.pre = (long long*)(base + (head + 1) / 2 * 2);
+  v.pre = (long long*)(base + gram_pre_at(T));
+  v.mask[0] = base + gram_mask_at(T);
+  v.mask[1] = v.mask[0] + 16 * (size_t)n0 * n0;
   return v;
 }
 __device__ __forceinline__ GramView gram_view(int* base, const GramPlan& pl) {
@@ -358,12 +357,12 @@ __global__ __launch_bounds__(NT) void k_gram_prep(FacArgs f0, const T* A0, int64
       nz |= x != 0.0;
     }
   }
-  // the block's 64 columns join the envelope of its 128-row block (a NaN
-  // counts as nonzero; integer min and max do not depend on the order)
-  if (__syncthreads_or(nz) && threadIdx.x == 0) {
+  // each wave's vote whether its part of the block holds a nonzero entry
+  // (a NaN counts as nonzero); k_gram_plan turns the votes into envelopes
+  const int any = __any(nz) ? 1 : 0;
+  if ((threadIdx.x & 63) == 0) {
     const GramView v = gram_view(f.genv, pl);
-    atomicMin(&v.emin[side][i0 >> 7], k0 >> 6);
-    atomicMax(&v.emax[side][i0 >> 7], (k0 >> 6) + 1);
+    v.mask[side][((int64_t)(i0 >> 6) * nt + (k0 >> 6)) * 4 + (threadIdx.x >> 6)] = any;
   }
 }
 
@@ -382,34 +381,41 @@ __device__ __forceinline__ void gram_issue(const double* Sp, const double* Sq, i
   }
 }
 
-// The envelopes start empty (first past last).
-template <bool BAT>
-__global__ __launch_bounds__(NT) void k_gram_env_init(FacArgs f0, GramPlan pl, BatchCtx bc) {
-  const FacProb* pb = bat_prob<BAT>(bc);
-  const FacArgs& f = BAT ? pb->base->f : f0;
-  const GramView v = gram_view(f.genv, pl);
-  for (int i = threadIdx.x; i < pl.n0; i += NT) {
-    v.emin[0][i] = 0x7fffffff;
-    v.emax[0][i] = 0;
-  }
-  for (int i = threadIdx.x; i < pl.n1; i += NT) {
-    v.emin[1][i] = 0x7fffffff;
-    v.emax[1][i] = 0;
-  }
-}
-
 // Every tile's chunk range from the envelopes of its two row blocks, the
 // prefix sum of the unit counts, and the number of ranges: the launch grid,
 // or fewer so that a range is at least as long as the longest tile.
 constexpr int PLT = 1024;
+constexpr int PLE = 512;  // 128-row blocks per side (dimensions up to 65536)
 template <bool BAT>
 __global__ __launch_bounds__(PLT) void k_gram_plan(FacArgs f0, GramPlan pl, BatchCtx bc) {
-  __shared__ long long part[PLT];
+  __shared__ long long scan[2][PLT];
   __shared__ int mx[PLT];
+  __shared__ int env[2][2][PLE];  // [side][first, one past last][128-row block]
   const FacProb* pb = bat_prob<BAT>(bc);
   const FacArgs& f = BAT ? pb->base->f : f0;
   const GramView v = gram_view(f.genv, pl);
   const int T = pl.t0 + pl.t1, t = threadIdx.x;
+  // envelopes of the 128-row blocks from the votes of the panel's 64 x 64
+  // blocks (start empty: first past last)
+  for (int i = t; i < 2 * PLE; i += PLT) {
+    env[i / PLE][0][i % PLE] = 0x7fffffff;
+    env[i / PLE][1][i % PLE] = 0;
+  }
+  __syncthreads();
+  for (int side = 0; side < 2; ++side) {
+    const int nk = 2 * (side ? pl.n1 : pl.n0);  // 64 x 64 blocks per panel row and column
+    const int4* votes = (const int4*)v.mask[side];
+    for (int e = t; e < nk * nk; e += PLT) {
+      const int4 q = votes[e];
+      if (q.x | q.y | q.z | q.w) {
+        atomicMin(&env[side][0][(e / nk) >> 1], e % nk);
+        atomicMax(&env[side][1][(e / nk) >> 1], e % nk + 1);
+      }
+    }
+  }
+  __syncthreads();
+  auto emin = [&](int side, int b) { return env[side][0][b]; };
+  auto emax = [&](int side, int b) { return env[side][1][b]; };
   const int per = (T + PLT - 1) / PLT, a0 = min(T, t * per), a1 = min(T, a0 + per);
   long long sum = 0;
   int most = 0;
@@ -417,7 +423,7 @@ __global__ __launch_bounds__(PLT) void k_gram_plan(FacArgs f0, GramPlan pl, Batc
     const int side = i < pl.t0 ? 0 : 1;
     int bp, bq;
     tri_index(side ? i - pl.t0 : i, bp, bq);
-    const int lo = max(v.emin[side][bp], v.emin[side][bq]), hi = min(v.emax[side][bp], v.emax[side][bq]);
+    const int lo = max(emin(side, bp), emin(side, bq)), hi = min(emax(side, bp), emax(side, bq));
     const bool empty = hi <= lo;
     v.clo[i] = empty ? 0 : 2 * lo;  // an envelope block is two 32-deep chunks
     v.chi[i] = empty ? 0 : 2 * hi;
@@ -425,24 +431,27 @@ __global__ __launch_bounds__(PLT) void k_gram_plan(FacArgs f0, GramPlan pl, Batc
     sum += cnt;
     most = max(most, cnt);
   }
-  part[t] = sum;
+  // inclusive scan of the threads' sums (Hillis-Steele) and the largest tile
+  scan[0][t] = sum;
   mx[t] = most;
   __syncthreads();
-  if (t == 0) {
-    long long run = 0;
-    int m = 1;
-    for (int i = 0; i < PLT; ++i) {
-      const long long x = part[i];
-      part[i] = run;
-      run += x;
-      m = max(m, mx[i]);
-    }
-    *v.U = run;
-    *v.Geff = (int)max(1LL, min((long long)pl.G, run / m));
-    v.pre[T] = run;
+  int cur = 0;
+  for (int off = 1; off < PLT; off <<= 1) {
+    const long long x = scan[cur][t] + (t >= off ? scan[cur][t - off] : 0);
+    const int y = t + off < PLT ? max(mx[t], mx[t + off]) : mx[t];
+    __syncthreads();
+    scan[cur ^ 1][t] = x;
+    mx[t] = y;  // mx[0] ends as the maximum
+    cur ^= 1;
+    __syncthreads();
   }
-  __syncthreads();
-  long long run = part[t];
+  const long long total = scan[cur][PLT - 1];
+  if (t == 0) {
+    *v.U = total;
+    *v.Geff = (int)max(1LL, min((long long)pl.G, total / max(mx[0], 1)));
+    v.pre[T] = total;
+  }
+  long long run = scan[cur][t] - sum;  // exclusive
   for (int i = a0; i < a1; ++i) {
     v.pre[i] = run;
     run += v.chi[i] > v.clo[i] ? v.chi[i] - v.clo[i] : 1;
@@ -1446,10 +1455,6 @@ static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq
   }
   if (fast) {
     const GramPlan pl = gram_plan(f.m, f.n, fast, f.cus);
-    go(1, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
-      constexpr bool BT = decltype(bat)::value;
-      hipLaunchKernelGGL(HIP_KERNEL_NAME(k_gram_env_init<BT>), g, dim3(NT), 0, st, a, pl, bc);
-    });
     go(nprep, s, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
       constexpr bool BT = decltype(bat)::value;
       if (dt == GPTQ2D_F32)

@@ -54,6 +54,73 @@ def test_factors_lower_triangular_closed_form():
     _factor_close(res["U"], np.diag(np.diag(B)) @ sla.solve_triangular(B, np.eye(90)), 1e-11)
 
 
+def _envelope_bases(kind, m, n, seed):
+    """Bases whose Gram panels have the structures the Gram's envelope meets:
+    block-diagonal A (128-blocks: every Gram tile off the block diagonal is
+    exactly zero) with banded upper B; lower-triangular A with upper B
+    (envelopes from opposite ends); dense A and B (the whole range)."""
+    rng = np.random.default_rng([77, seed, m, n])
+
+    def chol_block(d):
+        W = rng.standard_normal((2 * d, d))
+        return np.linalg.cholesky(W.T @ W / (2 * d) + 0.05 * np.eye(d)).T
+
+    def banded(d, bw):
+        T = np.triu(rng.standard_normal((d, d)) / np.sqrt(bw))
+        T = np.tril(T, bw)
+        T[np.diag_indices(d)] = np.exp(rng.uniform(np.log(0.5), np.log(2.0), size=d))
+        return T
+
+    if kind == "blockdiag":
+        A = np.zeros((m, m))
+        for b in range(0, m, 128):
+            A[b:b + 128, b:b + 128] = chol_block(128)
+        B = banded(n, 100)
+    elif kind == "lower":
+        A = chol_block(m).T
+        B = chol_block(n)
+    else:
+        A = rng.standard_normal((m, m)) / np.sqrt(m) + 2.0 * np.eye(m)
+        B = rng.standard_normal((n, n)) / np.sqrt(n) + 2.0 * np.eye(n)
+    X = 3.0 * rng.standard_normal((m, n))
+    return wl.Problem(f"envelope-{kind}-{m}x{n}", X, A, B, "f64")
+
+
+@pytest.mark.parametrize("kind", ["blockdiag", "lower", "general"])
+@pytest.mark.parametrize("m,n", [(384, 256), (256, 640)])
+def test_gram_envelope_structures(kind, m, n):
+    """Fast-path Grams (dimensions multiples of 128) on bases whose panels
+    have zero blocks: the factors against the oracle's, the sweep replayed
+    under the GPU's factors and the objective against the definition. The
+    handle first factors a dense problem, so its Gram buffer holds nonzero
+    values; the block-diagonal basis must then give a block-diagonal L (the
+    Gram tiles with an empty envelope are written as zeros)."""
+    p = _envelope_bases(kind, m, n, 1)
+    X, A, B = p.widened()
+    dense = _envelope_bases("general", m, n, 2)
+    f = binding.Factors(m, n)
+    f.compute(pr.to_dev(dense.A), pr.to_dev(dense.B))
+    binding.gptq2d_factor_check(f.handle)
+    f.compute(pr.to_dev(p.A), pr.to_dev(p.B))
+    binding.gptq2d_factor_check(f.handle)
+    Z, Y, obj = binding.round_matrix(f, pr.to_dev(p.X))
+    Lg, Ug, lamLg, lamUg = (t.cpu().numpy() for t in f.export())
+    Zg, Yg, objg = Z.cpu().numpy(), Y.cpu().numpy(), float(obj.cpu()[0])
+    f.close()
+    L, lamL, U, lamU = oracle.factors(A, B)
+    _factor_close(Lg, L, 1e-10)
+    _factor_close(Ug, U, 1e-10)
+    np.testing.assert_allclose(lamLg, lamL, rtol=1e-10)
+    np.testing.assert_allclose(lamUg, lamU, rtol=1e-10)
+    if kind == "blockdiag":
+        blk = np.arange(m) // 128
+        assert np.all(Lg[blk[:, None] != blk[None, :]] == 0.0)
+    Zo, Yo, c, hard = pr.replay(p, Lg, Ug, Zg)
+    pr.assert_replay_pass(p, c, hard, m * n)
+    assert np.abs(Yg - Yo).max() <= 1e-9
+    pr.assert_objective(p, objg, oracle.objective(X, Zo, A, B))
+
+
 @pytest.mark.parametrize("m,n", SHAPES)
 @pytest.mark.parametrize("dtype", ["f64", "f32"])
 def test_sweep_with_imported_factors(m, n, dtype):
