@@ -107,3 +107,113 @@ def blocked_sweep(X: torch.Tensor, L: torch.Tensor, U: torch.Tensor, w: int = 16
             V = torch.bmm(Cw[:, None, :].contiguous(), Uw.contiguous())[:, 0, :]
             Y[is_, :] += torch.where(later[is_, :], V, torch.zeros((), dtype=dt, device=dev))
     return Z, Y, E
+
+
+def skew_stride(m: int, n: int) -> int:
+    """Row stride r = 2m + n - 2 of the padded skew array (Sec. 5): m - 1
+    positions on either side of the n-wide band, where a matrix row line
+    (stride r + 1) overhangs at its ends."""
+    return 2 * m + n - 2
+
+
+def skew_matrix(flat: torch.Tensor, m: int, n: int) -> torch.Tensor:
+    """The m x n matrix held in a padded skew array, as a strided view: entry
+    (i, j) sits in row s = i + j at position m - 1 + j, i.e. at
+    i r + (m - 1) + j (r + 1) (Sec. 5, the construction)."""
+    r = skew_stride(m, n)
+    return flat.as_strided((m, n), (r, r + 1), m - 1)
+
+
+def blocked_sweep_skew(X: torch.Tensor, L: torch.Tensor, U: torch.Tensor, w: int = 16,
+                       col_chunk: int | None = None, arrays: dict | None = None):
+    """Algorithm 4 with Y, Z, C and E in the padded skew layout of Sec. 5.
+
+    Every access of the sweep is a slice with fixed strides: anti-diagonal s
+    is a contiguous piece of row s; the fold and the push down go to the
+    rows below it at the same positions (strides r, 1) and the push right
+    one position further per row (strides r + 1, 1); the down flush reads
+    each matrix column's window of w anti-diagonals of E as a stride-r line
+    and the right flush each matrix row's window of C as a stride-(r + 1)
+    line. Index ranges outside the matrix are skipped (their updates are
+    zero), so the padding cells stay zero and the flush windows read zeros
+    there. Returns Z, Y, E as m x n matrices; the same values as
+    blocked_sweep, which keeps the natural layout and addresses
+    anti-diagonals by index tensors. If arrays is a dict, it receives the
+    flat skew arrays ("Y", "Z", "C", "E")."""
+    m, n = X.shape
+    dev, dt = X.device, X.dtype
+    r = skew_stride(m, n)
+    S = m + n - 1
+    # rows beyond the last anti-diagonal absorb the zero updates of pushes
+    # that leave the matrix past its last rows or columns
+    size = (S + w + 1) * r
+    Yf = torch.zeros(size, dtype=dt, device=dev)
+    Cf = torch.zeros_like(Yf)
+    Ef = torch.zeros_like(Yf)
+    Zf = torch.zeros_like(Yf)
+    Yd, Cd, Ed, Zd = (skew_matrix(t, m, n) for t in (Yf, Cf, Ef, Zf))
+    Yd.copy_(X)
+    chunk = col_chunk or max(1, (1 << 25) // (max(m, n) * w))
+    ar_w = torch.arange(w, device=dev)
+    Lp = torch.zeros((m, m + 2 * w), dtype=dt, device=dev)
+    Lp[:, w:w + m] = L
+    Up = torch.zeros((n + 2 * w, n), dtype=dt, device=dev)
+    Up[w:w + n, :] = U
+    ii = torch.arange(m, device=dev)[:, None]
+    jj = torch.arange(n, device=dev)[None, :]
+    zero = torch.zeros((), dtype=dt, device=dev)
+    for s0 in range(0, S, w):
+        s1 = min(s0 + w - 1, S - 1)
+        for s in range(s0, s1 + 1):
+            jlo, jhi = max(0, s - m + 1), min(s, n - 1)
+            nt = jhi - jlo + 1
+            base = s * r + m - 1 + jlo  # anti-diagonal s: Yf[base : base + nt], column j = jlo + t
+            J = torch.arange(jlo, jhi + 1, device=dev)
+            I = s - J
+            y = Yf[base:base + nt]
+            z = torch.round(y)
+            e = z - y
+            Zf[base:base + nt] = z
+            Ef[base:base + nt] = e
+            D = s1 - s
+            d = torch.arange(D + 1, device=dev)[:, None]
+            R = I[None, :] + d  # target rows i + d (rows of the view)
+            ok = R < m
+            M = torch.where(ok, L[torch.where(ok, R, 0), I[None, :]] * e[None, :], zero)
+            # fold (d = 0: C_ij gets E_ij, L_ii = 1) and push down: the rows below, same positions
+            Cf.as_strided((D + 1, nt), (r, 1), base).add_(M)
+            if D > 0:
+                Yf.as_strided((D, nt), (r, 1), base + r).add_(M[1:])
+                Q = J[None, :] + d[1:]  # target columns j + d
+                okq = Q < n
+                V = torch.where(okq, Cf[base:base + nt][None, :] * U[J[None, :], torch.where(okq, Q, 0)], zero)
+                # push right: one position further per row below
+                Yf.as_strided((D, nt), (r + 1, 1), base + r + 1).add_(V)
+        if s1 == S - 1:
+            break
+        wb = s1 - s0 + 1
+        later = (ii + jj) > s1
+        # ---- down flush: column j's window of the block, E(s0 + d - j, j), d < wb
+        E2 = Ef.as_strided((n, wb), (1, r), s0 * r + m - 1)
+        M = torch.empty((m, n), dtype=dt, device=dev)
+        for c0 in range(0, n, chunk):
+            js = torch.arange(c0, min(n, c0 + chunk), device=dev)
+            # rows outside the matrix land in the zero padding (clamped there)
+            cols = ((s0 - js)[:, None] + ar_w[None, :wb] + w).clamp(0, m + 2 * w - 1)
+            Lw = Lp[:, cols]  # m x nj x wb: the shifting windows of L
+            M[:, js] = torch.bmm(Lw.permute(1, 0, 2).contiguous(), E2[js][:, :, None].contiguous())[:, :, 0].T
+        M = torch.where(later, M, zero)
+        Cd.add_(M)
+        Yd.add_(M)
+        # ---- right flush: row i's window of the block, C(i, s0 - i + d), read
+        # as the stride-(r + 1) lines in reverse row order and flipped back
+        Cw = Cf.as_strided((m, wb), (1, r + 1), s0 * (r + 1)).flip(0)
+        for r0_ in range(0, m, chunk):
+            is_ = torch.arange(r0_, min(m, r0_ + chunk), device=dev)
+            rows = ((s0 - is_)[:, None] + ar_w[None, :wb] + w).clamp(0, n + 2 * w - 1)
+            Uw = Up[rows, :]  # ni x wb x n: the shifting windows of U
+            V = torch.bmm(Cw[is_][:, None, :].contiguous(), Uw.contiguous())[:, 0, :]
+            Yd[is_, :] += torch.where(later[is_, :], V, zero)
+    if arrays is not None:
+        arrays.update(Y=Yf, Z=Zf, C=Cf, E=Ef)
+    return Zd.clone(), Yd.clone(), Ed.clone()

@@ -1,9 +1,10 @@
 """The paper's array-framework realisation of the sweep (Sec. 4.3, Algorithm 4;
-array_baseline.py, the comparison point timed by bench.py --array-baseline)
-run on the GPU: its Z passes the oracle's replay (Algorithm 5) and equals the
-HIP library's Z on the same problem and the same factors. The two share no
-code: one is batched PyTorch tensor operations, the other the library's
-kernels through the C ABI."""
+array_baseline.py, the comparison point timed by bench.py --array-baseline),
+in the natural layout and in the padded skew layout of Sec. 5, run on the
+GPU: its Z passes the oracle's replay (Algorithm 5) and equals the HIP
+library's Z on the same problem and the same factors. The two share no code:
+one is batched PyTorch tensor operations, the other the library's kernels
+through the C ABI."""
 import numpy as np
 import pytest
 import torch
@@ -21,18 +22,20 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.parametrize("m,n,w,kind", [(64, 64, 16, "wishart"), (100, 90, 8, "general"),
                                         (130, 70, 32, "wishart"), (37, 150, 1, "general"),
                                         (70, 60, 200, "wishart")])
-def test_array_baseline_on_device(m, n, w, kind):
+@pytest.mark.parametrize("layout", ["natural", "skew"])
+def test_array_baseline_on_device(m, n, w, kind, layout):
     p = wl.random_problem(m, n, 11, "f64", kind)
     X, A, B = p.widened()
     L, lamL, U, lamU = oracle.factors(A, B)
     dev = torch.device("cuda")
-    Zt, Yt, Et = ab.blocked_sweep(torch.from_numpy(X).to(dev), torch.from_numpy(L).to(dev),
-                                  torch.from_numpy(U).to(dev), w=w)
+    sweep = ab.blocked_sweep if layout == "natural" else ab.blocked_sweep_skew
+    Zt, Yt, Et = sweep(torch.from_numpy(X).to(dev), torch.from_numpy(L).to(dev),
+                       torch.from_numpy(U).to(dev), w=w)
     torch.cuda.synchronize()
     Z = Zt.cpu().numpy()
     Y = Yt.cpu().numpy()
     E = Et.cpu().numpy()
-    print(f"[array baseline on the device] {m} x {n}, w = {w}, {kind}", flush=True)
+    print(f"[array baseline on the device] {m} x {n}, w = {w}, {kind}, {layout} layout", flush=True)
     Zo, Yo, c, hard = oracle.round_nested(X, L, U, hint=Z.astype(np.int32), tau=1e-12)
     assert c["hard"] == 0 and c["window"] == 0 and c["range"] == 0, c
     assert np.abs(Y - Yo).max() <= 1e-12 * max(1.0, np.abs(Yo).max())
