@@ -217,3 +217,30 @@ def blocked_sweep_skew(X: torch.Tensor, L: torch.Tensor, U: torch.Tensor, w: int
     if arrays is not None:
         arrays.update(Y=Yf, Z=Zf, C=Cf, E=Ef)
     return Zd.clone(), Yd.clone(), Ed.clone()
+
+
+def skew_cells(m: int, n: int) -> int:
+    """Cells of one padded skew array: (m + n - 1)(2m + n - 2) for m n entries."""
+    return (m + n - 1) * skew_stride(m, n)
+
+
+def blocked_sweep_oriented(X: torch.Tensor, L: torch.Tensor, U: torch.Tensor, w: int = 16,
+                           orient: str = "auto", col_chunk: int | None = None):
+    """Algorithm 4 on the skew layout in the orientation Sec. 5 suggests:
+    rounding X^T under the swapped bases (B^T, A^T) is the same problem, with
+    feedback factors U^T (rows) and L^T (columns), and its skew arrays need
+    (m + n - 1)(2n + m - 2) cells instead of (m + n - 1)(2m + n - 2), fewer when
+    m > n. orient "auto" takes the orientation with the smaller first
+    dimension, "rows" keeps X, "columns" transposes. In the transposed sweep
+    the buffer is U^T E^T = (E U)^T: the right-hand buffer D = E U of
+    Appendix B, kept by rows instead of C = L E by columns. Returns Z, Y, E of
+    X (transposed back)."""
+    m, n = X.shape
+    if orient not in ("auto", "rows", "columns"):
+        raise ValueError(f"orient must be auto, rows or columns, not {orient!r}")
+    flip = orient == "columns" or (orient == "auto" and m > n)
+    if not flip:
+        return blocked_sweep_skew(X, L, U, w=w, col_chunk=col_chunk)
+    Zt, Yt, Et = blocked_sweep_skew(X.T.contiguous(), U.T.contiguous(), L.T.contiguous(), w=w,
+                                    col_chunk=col_chunk)
+    return Zt.T.contiguous(), Yt.T.contiguous(), Et.T.contiguous()

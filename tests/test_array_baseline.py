@@ -81,3 +81,29 @@ def test_skew_sweep_matches(m, n, w, kind):
     for key in ("E", "C", "Z"):
         assert not bool(arrays[key][~data].ne(0).any()), key
     assert data[:(m + n - 1) * r].sum() == m * n
+
+
+@pytest.mark.parametrize("m,n,w", [(40, 9, 8), (9, 40, 8), (33, 20, 4), (1, 25, 3), (25, 1, 3), (30, 30, 7)])
+def test_orientation_choice(m, n, w):
+    """Sec. 5's orientation choice: the transposed problem (X^T under B^T,
+    A^T, factors U^T and L^T, i.e. the mirror buffer D = E U) rounds to the
+    transpose of the same Z (Theorem 1; the oracle's replay passes in both
+    orientations), and "auto" picks the one with fewer skew cells."""
+    p = wl.random_problem(m, n, 4, "f64", "general")
+    X, A, B = p.widened()
+    L, lamL, U, lamU = oracle.factors(A, B)
+    # the transposed problem's factors are the transposed factors
+    Lt, _, Ut, _ = oracle.factors(B.T.copy(), A.T.copy())
+    assert np.abs(Lt - U.T).max() <= 1e-10 * max(1.0, np.abs(U).max())
+    assert np.abs(Ut - L.T).max() <= 1e-10 * max(1.0, np.abs(L).max())
+    args = (torch.from_numpy(X), torch.from_numpy(L), torch.from_numpy(U))
+    Zr, Yr, Er = ab.blocked_sweep_oriented(*args, w=w, orient="rows")
+    Zc, Yc, Ec = ab.blocked_sweep_oriented(*args, w=w, orient="columns")
+    for Z in (Zr, Zc):
+        Zo, Yo, c, hard = oracle.round_nested(X, L, U, hint=Z.numpy().astype(np.int32), tau=1e-12)
+        assert c["hard"] == 0 and c["range"] == 0 and c["window"] <= 1, c
+    assert int((Zr != Zc).sum()) <= 1
+    assert float((Yr - Yc).abs().max()) <= 1e-9 * max(1.0, float(Yr.abs().max()))
+    Za, _, _ = ab.blocked_sweep_oriented(*args, w=w, orient="auto")
+    assert torch.equal(Za, Zc if m > n else Zr)
+    assert ab.skew_cells(min(m, n), max(m, n)) <= ab.skew_cells(m, n)
