@@ -244,3 +244,38 @@ def blocked_sweep_oriented(X: torch.Tensor, L: torch.Tensor, U: torch.Tensor, w:
     Zt, Yt, Et = blocked_sweep_skew(X.T.contiguous(), U.T.contiguous(), L.T.contiguous(), w=w,
                                     col_chunk=col_chunk)
     return Zt.T.contiguous(), Yt.T.contiguous(), Et.T.contiguous()
+
+
+def implicit_sweep(X: torch.Tensor, L: torch.Tensor, U: torch.Tensor, rows: int | None = None):
+    """The implicit-Y form of Appendix B (Algorithm 6) with tensor operations:
+    only the buffer C = L E is kept. For every entry (i, j) of anti-diagonal
+    s at once, Y_ij = X_ij + C_i,1:j U_1:j,j, a row of C against a column of
+    U (U is unit upper, so the full row product is that prefix sum), then the
+    rounding; then each rounded entry adds L_i:m,i E_ij to column j of C (L is
+    unit lower: the full column is that suffix). Two batched products per
+    anti-diagonal, O(mn max(m, n)) in all. rows bounds the entries of an
+    anti-diagonal handled at once (memory: rows * max(m, n) values). Returns
+    Z, Y, E."""
+    m, n = X.shape
+    dev, dt = X.device, X.dtype
+    C = torch.zeros_like(X)
+    Z = torch.zeros_like(X)
+    Y = torch.zeros_like(X)
+    E = torch.zeros_like(X)
+    step = rows or max(1, (1 << 24) // max(m, n))
+    for s in range(m + n - 1):
+        jlo, jhi = max(0, s - m + 1), min(s, n - 1)
+        for a in range(jlo, jhi + 1, step):
+            J = torch.arange(a, min(jhi, a + step - 1) + 1, device=dev)
+            I = s - J
+            y = X[I, J] + (C[I, :] * U[:, J].T).sum(dim=1)
+            z = torch.round(y)
+            Z[I, J] = z
+            Y[I, J] = y
+            E[I, J] = z - y
+        # the column updates after the whole anti-diagonal is rounded (the
+        # entries of one anti-diagonal read none of each other's updates)
+        J = torch.arange(jlo, jhi + 1, device=dev)
+        I = s - J
+        C[:, J] += L[:, I] * E[I, J][None, :]
+    return Z, Y, E

@@ -204,6 +204,14 @@ def array_baseline_run(prob, sample: int, w: int, dev):
     torch.cuda.synchronize()
     t_skew = time.perf_counter() - t0
     mism_skew = int((Zs.to(torch.int32) != Zh).sum())
+    # the implicit-Y form of Appendix B (Algorithm 6), one buffer C = L E
+    ab.implicit_sweep(X64[:64, :64].contiguous(), L[:64, :64].contiguous(), U[:64, :64].contiguous())
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    Zi, _, _ = ab.implicit_sweep(X64, L, U)
+    torch.cuda.synchronize()
+    t_impl = time.perf_counter() - t0
+    mism_impl = int((Zi.to(torch.int32) != Zh).sum())
     f.close()
     m, n = prob.m, prob.n
     scale = (m * n * (m + n)) / (s_m * s_n * (s_m + s_n))
@@ -220,6 +228,8 @@ def array_baseline_run(prob, sample: int, w: int, dev):
         "z_mismatches_vs_hip": mism_skew,
         "natural_layout_sweep_s": t_arr,
         "natural_layout_z_mismatches_vs_hip": mism,
+        "implicit_y_sweep_s": t_impl,
+        "implicit_y_z_mismatches_vs_hip": mism_impl,
     }
 
 

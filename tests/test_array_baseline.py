@@ -107,3 +107,27 @@ def test_orientation_choice(m, n, w):
     Za, _, _ = ab.blocked_sweep_oriented(*args, w=w, orient="auto")
     assert torch.equal(Za, Zc if m > n else Zr)
     assert ab.skew_cells(min(m, n), max(m, n)) <= ab.skew_cells(m, n)
+
+
+# ---- the implicit-Y form (Appendix B, Algorithm 6) with tensor operations
+
+@pytest.mark.parametrize("m,n,kind,rows", [(1, 1, "wishart", None), (5, 7, "wishart", None), (33, 20, "general", 4),
+                                           (64, 70, "wishart", None), (100, 3, "general", 2), (3, 60, "diag", None)])
+def test_implicit_sweep_matches_oracle(m, n, kind, rows):
+    """Only C = L E is kept and Y_ij = X_ij + C_i,1:j U_1:j,j is read on demand:
+    the same Z under the oracle's replay, Y to 1e-12, Z - X = L E U, and the
+    same Z as the oracle's own Algorithm 6 and the blocked form; anti-diagonals
+    split into pieces of `rows` entries give the same result."""
+    p = wl.random_problem(m, n, 5, "f64", kind)
+    X, A, B = p.widened()
+    L, lamL, U, lamU = oracle.factors(A, B)
+    Zt, Yt, Et = ab.implicit_sweep(torch.from_numpy(X), torch.from_numpy(L), torch.from_numpy(U), rows=rows)
+    Z, Y, E = Zt.numpy(), Yt.numpy(), Et.numpy()
+    Zo, Yo, c, hard = oracle.round_nested(X, L, U, hint=Z.astype(np.int32), tau=1e-12)
+    assert c["hard"] == 0 and c["window"] == 0 and c["range"] == 0, c
+    assert np.abs(Y - Yo).max() <= 1e-12 * max(1.0, np.abs(Yo).max())
+    assert np.abs((Z - X) - L @ E @ U).max() <= 1e-11 * max(1.0, np.abs(X).max())
+    Zi, _, _, _ = oracle.round_implicit(X, L, U)
+    assert np.array_equal(Zi, Z.astype(np.int32))
+    Zb, _, _ = ab.blocked_sweep(torch.from_numpy(X), torch.from_numpy(L), torch.from_numpy(U), w=8)
+    assert torch.equal(Zb, Zt)

@@ -1,7 +1,7 @@
 """The paper's array-framework realisation of the sweep (Sec. 4.3, Algorithm 4;
 array_baseline.py, the comparison point timed by bench.py --array-baseline),
-in the natural layout and in the padded skew layout of Sec. 5, run on the
-GPU: its Z passes the oracle's replay (Algorithm 5) and equals the HIP
+in the natural layout and in the padded skew layout of Sec. 5, and the
+implicit-Y form of Appendix B (Algorithm 6), run on the GPU: its Z passes the oracle's replay (Algorithm 5) and equals the HIP
 library's Z on the same problem and the same factors. The two share no code:
 one is batched PyTorch tensor operations, the other the library's kernels
 through the C ABI."""
@@ -22,15 +22,18 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.parametrize("m,n,w,kind", [(64, 64, 16, "wishart"), (100, 90, 8, "general"),
                                         (130, 70, 32, "wishart"), (37, 150, 1, "general"),
                                         (70, 60, 200, "wishart")])
-@pytest.mark.parametrize("layout", ["natural", "skew"])
+@pytest.mark.parametrize("layout", ["natural", "skew", "implicit"])
 def test_array_baseline_on_device(m, n, w, kind, layout):
     p = wl.random_problem(m, n, 11, "f64", kind)
     X, A, B = p.widened()
     L, lamL, U, lamU = oracle.factors(A, B)
     dev = torch.device("cuda")
-    sweep = ab.blocked_sweep if layout == "natural" else ab.blocked_sweep_skew
-    Zt, Yt, Et = sweep(torch.from_numpy(X).to(dev), torch.from_numpy(L).to(dev),
-                       torch.from_numpy(U).to(dev), w=w)
+    args = (torch.from_numpy(X).to(dev), torch.from_numpy(L).to(dev), torch.from_numpy(U).to(dev))
+    if layout == "implicit":  # Algorithm 6 (Appendix B): no blocks, only C = L E kept
+        Zt, Yt, Et = ab.implicit_sweep(*args)
+    else:
+        sweep = ab.blocked_sweep if layout == "natural" else ab.blocked_sweep_skew
+        Zt, Yt, Et = sweep(*args, w=w)
     torch.cuda.synchronize()
     Z = Zt.cpu().numpy()
     Y = Yt.cpu().numpy()
