@@ -13,9 +13,16 @@ windows of w columns of L and w rows of U that shift with the receiving
 column or row. Indices are 0-based: anti-diagonal s holds the entries
 i + j = s, s = 0 .. m + n - 2.
 
-Ties of the rounding go to even (torch.round), as everywhere in this build.
-The factors are inputs: L unit lower (m x m) and U unit upper (n x n) of the
-inverse Grams, with L_ii = U_jj = 1.
+blocked_sweep keeps the natural layout and addresses anti-diagonals by index
+tensors; blocked_sweep_skew keeps the working matrices in the padded skew
+layout of Sec. 5, where every access is a fixed-stride slice;
+blocked_sweep_oriented adds Sec. 5's orientation choice (the transposed
+problem, whose buffer is the mirror D = E U of Appendix B); implicit_sweep
+is the implicit-Y form of Appendix B (Algorithm 6), which keeps only C = L E.
+
+Ties of the rounding go to even (torch.round), as in the library and the
+oracle. The factors are inputs: L unit lower (m x m) and U unit upper
+(n x n) of the inverse Grams, with L_ii = U_jj = 1.
 """
 from __future__ import annotations
 
