@@ -91,6 +91,8 @@ def _load():
         lib.orc_round_nested_corner.argtypes = [i, i, i, i, dp, dp, dp, ip, ctypes.c_double, ip, dp,
                                                 lp, lp, i]
         lib.orc_round_nested_corner.restype = i
+        lib.orc_round_nested_cols.argtypes = [i, i, i, dp, dp, dp, ip, ctypes.c_double, ip, dp, lp, lp, i]
+        lib.orc_round_nested_cols.restype = i
         lib.orc_objective.argtypes = [i, i, dp, ip, dp, dp]
         lib.orc_objective.restype = ctypes.c_double
         lib.orc_num_threads.argtypes = []
@@ -260,6 +262,27 @@ def round_gptq2d(X, L, U, hint=None, tau=0.0, hard_cap=64):
 
 def round_implicit(X, L, U, hint=None, tau=0.0, hard_cap=64):
     return _sweep("orc_round_implicit", X, L, U, hint, tau, hard_cap)
+
+
+def round_nested_columns(X, L, U, ncols):
+    """Algorithm 5 on the first ncols columns of the problem only: Z and the
+    corrected values of those columns (an error at (i, j) reaches only columns
+    >= j, Eq. rank-one-update, so they are the whole sweep's). Bounds the CPU
+    work of a large problem when the sweep is timed."""
+    X = _d(X)
+    L = _d(L)
+    U = _d(U)
+    m, n = X.shape
+    if L.shape != (m, m) or U.shape != (n, n):
+        raise ValueError("factor shape mismatch")
+    if not (0 <= ncols <= n):
+        raise ValueError("ncols out of range")
+    h, counts, hard = _replay_args(None, (m, n), 0.0, 64)
+    Z = np.zeros((m, n), dtype=np.int32)
+    Y = np.zeros((m, n))
+    _check(_load().orc_round_nested_cols(m, n, int(ncols), _dp(X), _dp(L), _dp(U), _ip(h), 0.0, _ip(Z),
+                                         _dp(Y), _lp(counts), _lp(hard), 64), "round_nested_cols")
+    return Z[:, :ncols].copy(), Y[:, :ncols].copy()
 
 
 def round_nested_corner(X, L, U, m1, n1, hint=None, tau=0.0, hard_cap=64):

@@ -360,9 +360,15 @@ int orc_round_kron(int m, int n, const double* X, const double* L, const double*
 /* Algorithm 5: nested column-major form (Appendix A) -- the cubic oracle    */
 /* ------------------------------------------------------------------------ */
 
-int orc_round_nested(int m, int n, const double* X, const double* L, const double* U,
-                     const int32_t* hint, double tau, int32_t* Z, double* Ypre, int64_t* counts,
-                     int64_t* hard_idx, int hard_cap) {
+/* Algorithm 5 on the first ncols columns only (0 <= ncols <= n): the sweep is
+ * column by column and an error at (i, j) reaches only columns >= j (Eq.
+ * rank-one-update), so these columns of Z and Ypre are those of the whole
+ * sweep; the later columns of Z and Ypre are left unwritten. This bounds the
+ * CPU work of a large problem for timing. */
+int orc_round_nested_cols(int m, int n, int ncols, const double* X, const double* L, const double* U,
+                          const int32_t* hint, double tau, int32_t* Z, double* Ypre, int64_t* counts,
+                          int64_t* hard_idx, int hard_cap) {
+  if (ncols < 0 || ncols > n) return ORC_ERR_RANGE;
   double* Y = (double*)malloc(sizeof(double) * (size_t)m * n);
   double* y = (double*)malloc(sizeof(double) * (size_t)m);
   if (!Y || !y) { free(Y); free(y); return ORC_ERR_NOMEM; }
@@ -371,7 +377,7 @@ int orc_round_nested(int m, int n, const double* X, const double* L, const doubl
   int64_t local[3];
   orc_replay_init(&rp, hint, tau, counts ? counts : local, hard_idx, hard_cap);
   int bad = 0;
-  for (int j = 0; j < n; ++j) {
+  for (int j = 0; j < ncols; ++j) {
     /* y <- Y[:, j]; one-dimensional sweep of the column under L */
     for (int i = 0; i < m; ++i) y[i] = Y[(size_t)i * n + j];
     for (int i = 0; i < m; ++i) {
@@ -395,6 +401,12 @@ int orc_round_nested(int m, int n, const double* X, const double* L, const doubl
   free(Y);
   free(y);
   return bad ? ORC_ERR_RANGE : ORC_OK;
+}
+
+int orc_round_nested(int m, int n, const double* X, const double* L, const double* U,
+                     const int32_t* hint, double tau, int32_t* Z, double* Ypre, int64_t* counts,
+                     int64_t* hard_idx, int hard_cap) {
+  return orc_round_nested_cols(m, n, n, X, L, U, hint, tau, Z, Ypre, counts, hard_idx, hard_cap);
 }
 
 /* Nested form restricted to the leading block rows [0, m1) x columns [0, n1):

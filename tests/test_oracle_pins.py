@@ -380,6 +380,26 @@ def test_corner_is_self_contained():
     assert np.abs(Yc - Y[:9, :13]).max() < 1e-12
 
 
+def test_leading_columns_are_self_contained():
+    """Algorithm 5 stopped after k columns (the bounded sample the benchmark
+    times) gives the whole sweep's first k columns: an error at (i, j) reaches
+    only columns >= j (Eq. rank-one-update). Checked against the full nested
+    sweep and against Algorithm 3, whose anti-diagonal order shares no loop
+    with it."""
+    X, A, B = _prob(23, 19, 8, "general")
+    L, _, U, _ = oracle.factors(A, B)
+    Z, Y, _, _ = oracle.round_nested(X, L, U)
+    Zg, _, _, _ = oracle.round_gptq2d(X, L, U)
+    assert np.array_equal(Z, Zg)
+    for k in (0, 1, 7, 19):
+        Zk, Yk = oracle.round_nested_columns(X, L, U, k)
+        assert Zk.shape == (23, k) and Yk.shape == (23, k)
+        assert np.array_equal(Zk, Z[:, :k]) and np.array_equal(Zk, Zg[:, :k])
+        assert np.array_equal(Yk, Y[:, :k])
+    with pytest.raises(ValueError):
+        oracle.round_nested_columns(X, L, U, 20)
+
+
 # --------------------------------------------------------------------------
 # Synchronised replay
 # --------------------------------------------------------------------------
