@@ -665,10 +665,14 @@ size_t gram_env_ints(int m, int n) {
 //
 // Blocked over 16 x 16 sub-blocks held in LDS. For each diagonal sub-block k:
 // one wave factors it and inverts the factor in registers (16 pivots, each
-// broadcast by DPP); the other sub-blocks
-// of column k are solved against that inverse and the trailing sub-blocks
-// updated, both as 16 x 16 MFMA products. The inverse of the whole factor is
-// then assembled block row by block row:
+// broadcast by DPP); the other sub-blocks of column k are solved against that
+// inverse and the trailing sub-blocks updated, both as 16 x 16 MFMA products.
+// The wave that owns the next diagonal sub-block updates it from its own
+// panel first and factors it while the other waves finish their trailing
+// updates, so only one panel product and one update lie between two
+// factorisations. The inverse of the whole factor is assembled block row by
+// block row, each row as soon as its diagonal block is inverted, by the waves
+// left idle:
 //   W_ij = -W_ii (sum_{k=j}^{i-1} L_ik W_kj).
 // A pivot that is not positive and finite raises FLAG_SINGULAR and is
 // replaced by 1 so the remaining work stays finite.
@@ -722,35 +726,32 @@ __device__ __forceinline__ void d4_store(const d4& acc, double* P, int ld) {
 }
 
 // v of lane `lane` (0..15, a constant after unrolling) of every 16-lane row,
-// broadcast to the whole row (DPP row_newbcast), for a double.
+// broadcast to the whole row (DPP row_newbcast, one 64-bit move).
 __device__ __forceinline__ double bcast16(double v, int lane) {
-  const long long x = __double_as_longlong(v);
-  int lo = (int)x, hi = (int)(x >> 32);
-#define G2D_BC(L_)                                                  \
-  case L_:                                                          \
-    lo = __builtin_amdgcn_mov_dpp(lo, 0x150 + (L_), 0xf, 0xf, false); \
-    hi = __builtin_amdgcn_mov_dpp(hi, 0x150 + (L_), 0xf, 0xf, false); \
-    break;
   switch (lane) {
+#define G2D_BC(L_) \
+  case L_:         \
+    return __builtin_amdgcn_mov_dpp(v, 0x150 + (L_), 0xf, 0xf, false);
     G2D_BC(0) G2D_BC(1) G2D_BC(2) G2D_BC(3) G2D_BC(4) G2D_BC(5) G2D_BC(6) G2D_BC(7)
     G2D_BC(8) G2D_BC(9) G2D_BC(10) G2D_BC(11) G2D_BC(12) G2D_BC(13) G2D_BC(14) G2D_BC(15)
-    default: break;
-  }
 #undef G2D_BC
-  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+    default: return v;
+  }
 }
 
 // Factor the 16 x 16 diagonal sub-block at A (stride lda, lower part valid)
 // in place and write its inverse to W (stride ldw). One wave; lane x of
 // every 16-lane row holds column x of the symmetric block and column x of
 // the inverse in registers, and every broadcast is a DPP broadcast of one
-// lane within the row. Pivot j:
-//   - the column j of L is broadcast: L[r][j] = S[r][j] / sqrt(S[j][j]);
-//   - lane x's entry j becomes L[x][j] (by symmetry), and every lane
-//     subtracts L[r][j] L[x][j] from its entries r > j (right-looking
-//     Cholesky; entries r > x of lane x are never used again);
-//   - every lane advances the column-oriented forward substitution of
-//     L W = I with the same column: w[j] /= L[j][j], w[r] -= L[r][j] w[j].
+// lane within the row. Pivot j, with s = 1 / sqrt(S[j][j]):
+//   - lane x's entry j becomes L[x][j] = S[x][j] s (x >= j), and entry j of
+//     its column of the inverse is divided by L[j][j];
+//   - every lane subtracts L[r][j] L[x][j] = S[r][j] (S[x][j] s^2) from its
+//     entries r > j (right-looking Cholesky; entries r > x of lane x are
+//     never used again), with S[r][j] broadcast from lane j, and advances the
+//     column-oriented forward substitution of L W = I by the same column;
+//   - entry j + 1 goes first, so that the next pivot's square root overlaps
+//     the remaining updates.
 // At the end lane x holds row x of L (entries 0..x) and column x of W.
 __device__ void chol_inv16(double* A, int lda, double* W, int ldw, int* flags) {
   int l = threadIdx.x & 63;
@@ -766,27 +767,37 @@ __device__ void chol_inv16(double* A, int lda, double* W, int ldw, int* flags) {
   }
   __builtin_amdgcn_wave_barrier();
   bool bad = false;
-#pragma unroll
-  for (int j = 0; j < DS; ++j) {
-    double piv = bcast16(a[j], j);
+  auto pivot_rs = [&](double piv) {
     const bool ok = piv > 0.0 && isfinite(piv);
     bad |= !ok;
-    piv = ok ? piv : 1.0;
-    const double rs = rsqrt_nr(piv);
+    return rsqrt_nr(ok ? piv : 1.0);
+  };
+  double rs = pivot_rs(bcast16(a[0], 0));
+#pragma unroll
+  for (int j = 0; j < DS; ++j) {
+    const double rs2 = rs * rs;
+    const double c = -a[j] * rs2, cw = -w[j] * rs2;
     a[j] *= rs;
     w[j] *= rs;
-    const double na = -a[j], nw = -w[j];
-    double lc[DS];
-#pragma unroll
-    for (int r = j + 1; r < DS; ++r) lc[r] = bcast16(a[r], j) * rs;
-#pragma unroll
-    for (int r = j + 1; r < DS; ++r) {
-      a[r] = fma(lc[r], na, a[r]);
-      w[r] = fma(lc[r], nw, w[r]);
+    double rs_next = 1.0;
+    if (j + 1 < DS) {
+      const double b = bcast16(a[j + 1], j);
+      a[j + 1] = fma(b, c, a[j + 1]);
+      w[j + 1] = fma(b, cw, w[j + 1]);
+      // (an empty asm keeps each update of the inverse in place: left free,
+      // the compiler defers them past the loop and parks the broadcasts in
+      // spare registers, one more move per entry)
+      asm volatile("" : "+v"(w[j + 1]));
+      rs_next = pivot_rs(bcast16(a[j + 1], j + 1));
     }
-#ifndef G2D_NO_PIVOT_FENCE
-    __builtin_amdgcn_sched_barrier(0);  // keep each pivot's broadcasts local (register pressure)
-#endif
+#pragma unroll
+    for (int r = j + 2; r < DS; ++r) {
+      const double b = bcast16(a[r], j);
+      a[r] = fma(b, c, a[r]);
+      w[r] = fma(b, cw, w[r]);
+      asm volatile("" : "+v"(w[r]));
+    }
+    rs = rs_next;
   }
   if (bad && l == 0) raise_flag(flags, FLAG_SINGULAR);
   // after pivot j, a[j] of lane x is L[x][j] (x >= j): each lane holds row x of
@@ -831,41 +842,51 @@ __device__ void diag_tile(const Side& sd, int kb, int* flags, DiagSmem& ds) {
     }
   }
   __syncthreads();
-  for (int k = 0; k < 4; ++k) {
+  // off-diagonal block row i of the inverse, block (i, w) by wave w < i:
+  // W_iw = -W_ii (sum_{m=w}^{i-1} L_im W_mw)
+  auto wrow = [&](int i) {
+    d4 acc = {0.0, 0.0, 0.0, 0.0};
+    for (int m = w; m < i; ++m) mfma_lds<DS, 0>(acc, &Am[DS * i][DS * m], LD, &Wm[DS * m][DS * w], LD, 1.0);
+    d4_store(acc, &Tm[w][0][0], DS + 1);
+    __builtin_amdgcn_wave_barrier();
+    d4 acc2 = {0.0, 0.0, 0.0, 0.0};
+    mfma_lds<DS, 0>(acc2, &Wm[DS * i][DS * i], LD, &Tm[w][0][0], DS + 1, -1.0);
+    d4_store(acc2, &Wm[DS * i][DS * w], LD);
+  };
+  if (w == 0) chol_inv16(&Am[0][0], LD, &Wm[0][0], LD, flags);
+  __syncthreads();
+  for (int k = 0; k < 3; ++k) {
     const int o = DS * k;
-    if (w == k) chol_inv16(&Am[o][o], LD, &Wm[o][o], LD, flags);
-    __syncthreads();
     if (w > k) {  // panel: L_wk = A_wk W_kk^T
       d4 acc = {0.0, 0.0, 0.0, 0.0};
       mfma_lds<DS, 1>(acc, &Am[DS * w][o], LD, &Wm[o][o], LD, 1.0);
       __builtin_amdgcn_wave_barrier();
       d4_store(acc, &Am[DS * w][o], LD);
     }
+    if (w == k + 1) {  // the next diagonal block, from the wave's own panel: A_ww -= L_wk L_wk^T
+      __builtin_amdgcn_wave_barrier();
+      d4 acc;
+      d4_load(acc, &Am[DS * w][DS * w], LD);
+      mfma_lds<DS, 1>(acc, &Am[DS * w][o], LD, &Am[DS * w][o], LD, -1.0);
+      d4_store(acc, &Am[DS * w][DS * w], LD);
+    }
     __syncthreads();
-    if (w > k) {  // trailing: A_wj -= L_wk L_jk^T, k < j <= w
+    if (w == k + 1) {
+      chol_inv16(&Am[DS * w][DS * w], LD, &Wm[DS * w][DS * w], LD, flags);
+    } else if (w > k + 1) {  // trailing: A_wj -= L_wk L_jk^T, k < j <= w
       for (int j = k + 1; j <= w; ++j) {
         d4 acc;
         d4_load(acc, &Am[DS * w][DS * j], LD);
         mfma_lds<DS, 1>(acc, &Am[DS * w][o], LD, &Am[DS * j][o], LD, -1.0);
         d4_store(acc, &Am[DS * w][DS * j], LD);
       }
+    } else if (w < k) {  // block row k of the inverse (W_kk is ready)
+      wrow(k);
     }
     __syncthreads();
   }
-  // off-diagonal blocks of the inverse, block row by block row
-  for (int i = 1; i < 4; ++i) {
-    if (w < i) {
-      d4 acc = {0.0, 0.0, 0.0, 0.0};
-      for (int k = w; k < i; ++k)
-        mfma_lds<DS, 0>(acc, &Am[DS * i][DS * k], LD, &Wm[DS * k][DS * w], LD, 1.0);
-      d4_store(acc, &Tm[w][0][0], DS + 1);
-      __builtin_amdgcn_wave_barrier();
-      d4 acc2 = {0.0, 0.0, 0.0, 0.0};
-      mfma_lds<DS, 0>(acc2, &Wm[DS * i][DS * i], LD, &Tm[w][0][0], DS + 1, -1.0);
-      d4_store(acc2, &Wm[DS * i][DS * w], LD);
-    }
-    __syncthreads();
-  }
+  if (w < 3) wrow(3);
+  __syncthreads();
   double* dv = sd.dinv + (int64_t)kb * TB * TB;
 #pragma unroll
   for (int s = 0; s < 16; ++s) {
