@@ -1528,15 +1528,16 @@ static gptq2d_status factor_impl(Factors& f, const FacProb* tab, int count, gptq
     if (nfar > 0) {
       int units = 256;
       (void)hipDeviceGetAttribute(&units, hipDeviceAttributeMultiprocessorCount, f.device);
-      // a far update of a few tiles per compute unit leaves at least 32 units
+      // a far update of a few tiles per compute unit leaves at least 8 units
       // to the diagonal blocks, panels and near updates beside it (measured
-      // best at 4096), and spreads its tiles evenly over as few work groups as
-      // the same number of rounds needs, so that the rest of the device stays
-      // free; a larger one is the longer of the two streams and takes every
-      // unit (a batch fills the device by itself: one tile per work group)
+      // best at 4096 among 0 to 48), and spreads its tiles evenly over as few
+      // work groups as the same number of rounds needs, so that the rest of
+      // the device stays free; a larger one is the longer of the two streams
+      // and takes every unit (a batch fills the device by itself: one tile
+      // per work group)
       int grid = nfar;
       if (!tab && nfar <= 4 * units) {
-        const int rounds = (nfar + units - 33) / (units - 32);
+        const int rounds = (nfar + units - 9) / (units - 8);
         grid = (nfar + rounds - 1) / rounds;
       }
       go(grid, st0, [&](auto bat, dim3 g, BatchCtx bc, hipStream_t st) {
