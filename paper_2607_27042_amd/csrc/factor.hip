@@ -900,9 +900,10 @@ template <bool BAT>
 __global__ __launch_bounds__(NT) void k_diag(FacArgs f0, int kb, BatchCtx bc) {
   __shared__ DiagSmem ds;
   const FacArgs& f = BAT ? bat_prob<BAT>(bc)->base->f : f0;
-  const Side& sd = f.s[bat_block<BAT>(bc)];
+  const Side sd = f.s[bat_block<BAT>(bc)];  // a copy: the stores below cannot alias it
+  int* const flags = f.flags;
   if (kb >= sd.nb) return;
-  diag_tile(sd, kb, f.flags, ds);
+  diag_tile(sd, kb, flags, ds);
 }
 
 // ---------------------------------------------------------------------------
