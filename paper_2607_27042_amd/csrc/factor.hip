@@ -1012,7 +1012,7 @@ __global__ __launch_bounds__(NT) void k_update(FacArgs f0, UpdRange r, BatchCtx 
     else if (b == nq0 + ns0) b = 1;
   }
   const bool s1 = b >= nq0 + ns0;
-  const Side& sd = s1 ? f.s[1] : f.s[0];
+  const Side sd = s1 ? f.s[1] : f.s[0];  // a copy: the stores below cannot alias it
   if (s1) b -= nq0 + ns0;
   int nq, ns;
   upd_counts(sd, r, nq, ns);
