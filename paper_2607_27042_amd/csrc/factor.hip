@@ -750,8 +750,9 @@ __device__ __forceinline__ double bcast16(double v, int lane) {
 //     entries r > j (right-looking Cholesky; entries r > x of lane x are
 //     never used again), with S[r][j] broadcast from lane j, and advances the
 //     column-oriented forward substitution of L W = I by the same column;
-//   - entry j + 1 goes first, so that the next pivot's square root overlaps
-//     the remaining updates.
+//   - entry j + 1 goes first, so that the next pivot's square root can be
+//     scheduled between the remaining updates, whose broadcasts are all
+//     issued before their multiply-adds.
 // At the end lane x holds row x of L (entries 0..x) and column x of W.
 __device__ void chol_inv16(double* A, int lda, double* W, int ldw, int* flags) {
   int l = threadIdx.x & 63;
@@ -784,19 +785,22 @@ __device__ void chol_inv16(double* A, int lda, double* W, int ldw, int* flags) {
       const double b = bcast16(a[j + 1], j);
       a[j + 1] = fma(b, c, a[j + 1]);
       w[j + 1] = fma(b, cw, w[j + 1]);
-      // (an empty asm keeps each update of the inverse in place: left free,
-      // the compiler defers them past the loop and parks the broadcasts in
-      // spare registers, one more move per entry)
-      asm volatile("" : "+v"(w[j + 1]));
       rs_next = pivot_rs(bcast16(a[j + 1], j + 1));
     }
+    double bb[DS];
+#pragma unroll
+    for (int r = j + 2; r < DS; ++r) bb[r] = bcast16(a[r], j);
 #pragma unroll
     for (int r = j + 2; r < DS; ++r) {
-      const double b = bcast16(a[r], j);
-      a[r] = fma(b, c, a[r]);
-      w[r] = fma(b, cw, w[r]);
-      asm volatile("" : "+v"(w[r]));
+      a[r] = fma(bb[r], c, a[r]);
+      w[r] = fma(bb[r], cw, w[r]);
     }
+    // an empty asm keeps the pivot's updates of the inverse inside the
+    // pivot: left free, the compiler defers them past the loop and parks the
+    // broadcasts in spare registers, one more move per entry
+    asm volatile("" : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]), "+v"(w[4]), "+v"(w[5]), "+v"(w[6]),
+                 "+v"(w[7]), "+v"(w[8]), "+v"(w[9]), "+v"(w[10]), "+v"(w[11]), "+v"(w[12]), "+v"(w[13]),
+                 "+v"(w[14]), "+v"(w[15]));
     rs = rs_next;
   }
   if (bad && l == 0) raise_flag(flags, FLAG_SINGULAR);
